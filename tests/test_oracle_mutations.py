@@ -1,0 +1,88 @@
+"""Plant plausible mistakes in copies of the oracle; the pins must catch each.
+
+Each case rewrites one line of an oracle module's source, executes the copy
+as a fresh module (the real oracle is untouched) and runs every pin on it.
+At least one pin has to fail, otherwise the pins would let that mistake
+through.
+"""
+
+import os
+import types
+
+import pytest
+
+import oracle_pins as pins
+
+ORACLE_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
+
+
+def _mutant(filename, old, new):
+    path = os.path.join(ORACLE_DIR, filename)
+    with open(path) as f:
+        src = f.read()
+    assert src.count(old) == 1, f"mutation anchor not unique in {filename}: {old!r}"
+    mod = types.ModuleType("mutant_" + filename[:-3])
+    exec(compile(src.replace(old, new), path, "exec"), mod.__dict__)
+    return mod
+
+
+def _all_pins(att, plan):
+    checks = [
+        lambda: pins.check_brute(att.attend),
+        lambda: pins.check_sdpa(att.full_causal_attention),
+        lambda: pins.check_closed_forms(att.full_causal_attention),
+        lambda: pins.check_zigzag_restore(att.full_causal_attention, att.rank_partial, plan.shard_plan),
+        lambda: pins.check_merge(att.full_causal_attention, att.attend, att.lse_merge),
+        lambda: pins.check_paged_prefix(att.full_causal_attention, att.rank_partial, att.gather_paged),
+        lambda: pins.check_plan(plan.shard_plan, plan.remaining_workload, plan.shard_plan_fast),
+    ]
+    failed = 0
+    for c in checks:
+        try:
+            c()
+        except Exception:
+            failed += 1
+    return failed
+
+
+ATTENTION_MUTATIONS = [
+    ("strict causal mask", "k_pos[None, :] <= q_pos[b0:b1, None]", "k_pos[None, :] < q_pos[b0:b1, None]"),
+    ("wrong softmax scale", "scale = 1.0 / math.sqrt(D)", "scale = 1.0 / D"),
+    ("GQA heads interleaved", "g = h // group", "g = h % Hkv"),
+    ("V used as keys", "x = (q[b0:b1, h, :] @ kg.T) * scale", "x = (q[b0:b1, h, :] @ vg.T) * scale"),
+    ("max dropped from LSE", "lse[idx, h] = mx[live] + np.log(denom)", "lse[idx, h] = np.log(denom)"),
+    ("output not normalised", "out_rows = (e @ vg) / denom[:, None]", "out_rows = (e @ vg)"),
+    ("merge weight sign", "np.exp(stack - safe_mx)", "np.exp(safe_mx - stack)"),
+    ("merge ignores the max", "lse = np.where(live, safe_mx + np.log(", "lse = np.where(live, 0 * safe_mx + np.log("),
+    ("block table ignored", "cache[table[j // block_tokens], j % block_tokens]", "cache[j // block_tokens, j % block_tokens]"),
+    ("suffix off by one", "suffix_ranges = [(P, P + R)]", "suffix_ranges = [(P + 1, P + R)]"),
+    ("suffix keys at wrong positions", "ps.append(np.arange(P + lo_i, P + hi_i, dtype=np.int64))",
+     "ps.append(np.arange(lo_i, hi_i, dtype=np.int64))"),
+]
+
+PLAN_MUTATIONS = [
+    ("second chunk off by one", "for chunk_id in (rank, 2 * C - 1 - rank):\n        start = chunk_id * s                      # suffix",
+     "for chunk_id in (rank, 2 * C - 2 - rank):\n        start = chunk_id * s                      # suffix"),
+    ("no padding", "padded = -(-R // (2 * C)) * (2 * C)", "padded = R"),
+    ("W drops the prefix term", "return R * P + R * (R + 1) // 2", "return R * (R + 1) // 2"),
+    ("diagonal not counted", "for _key in range(pos + 1):", "for _key in range(pos):"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", ATTENTION_MUTATIONS, ids=[m[0] for m in ATTENTION_MUTATIONS])
+def test_attention_mutation_is_caught(name, old, new):
+    from oracle import plan
+    att = _mutant("attention.py", old, new)
+    assert _all_pins(att, plan) >= 1, f"no pin catches: {name}"
+
+
+@pytest.mark.parametrize("name,old,new", PLAN_MUTATIONS, ids=[m[0] for m in PLAN_MUTATIONS])
+def test_plan_mutation_is_caught(name, old, new):
+    from oracle import attention
+    plan = _mutant("plan.py", old, new)
+    assert _all_pins(attention, plan) >= 1, f"no pin catches: {name}"
+
+
+def test_unmutated_oracle_passes_every_pin():
+    from oracle import attention, plan
+    assert _all_pins(attention, plan) == 0
