@@ -1,0 +1,214 @@
+/*
+ * cp_attn.h -- C ABI of libcpattn: one context-parallel (CP) rank's causal
+ * prefill attention on an AMD Instinct MI355X (gfx950).
+ *
+ * The method (arXiv 2609.04774, "Adaptive Context Parallelism for Production
+ * LLM Serving"):
+ *   Sec. 2.1  Causal attention softmax(QK^T/sqrt(d_h) + M)V, M_ij = 0 for
+ *             j <= i.  Zigzag CP: the sequence is padded to a multiple of 2C,
+ *             cut into 2C equal contiguous chunks, and rank k holds chunks k
+ *             and 2C-1-k; each rank attends its queries to every causally
+ *             visible key and the outputs are restored to the original order.
+ *   Sec. 2.2  With a prefix-cache hit L = P + R: only the R uncached tokens
+ *             are computed, attending to the P cached keys and to the earlier
+ *             uncached ones; the work is W(R,P) = RP + R(R+1)/2 pairs.
+ *   Sec. 7.1  The cached prefix is a sequence of fixed-size cache blocks.
+ *
+ * Conventions shared by every call:
+ *   - Tensors are dense, row-major, in device memory unless a pointer is
+ *     documented as host memory.  bf16 is IEEE bfloat16 stored as uint16.
+ *   - Positions: the cached prefix occupies global positions 0..P-1, the
+ *     uncached suffix P..P+R-1 (suffix index i <-> global position P+i).
+ *   - Zigzag is applied to the suffix only; padding sits at its end and is
+ *     never a row.  A rank's rows are compact: chunk `rank` first, then chunk
+ *     2C-1-rank, each in increasing position.
+ *   - Grouped-query attention: query head h reads KV head h / (Hq/Hkv).
+ *   - The head dimension D is 128; paged KV blocks hold 16 tokens.
+ *   - Partial outputs are normalised: O = sum_j e^{x_j - LSE} v_j over the
+ *     partial's keys, LSE = ln sum_j e^{x_j} (natural log, x_j = scale*q.k).
+ *     A row that sees no key has O = 0 and LSE = -inf.
+ *   - The caller owns every buffer and the stream.  No call allocates device
+ *     memory, synchronises the device, or keeps pointers after returning.
+ *     Launching calls are asynchronous on `stream` (a hipStream_t; NULL is the
+ *     null stream) and return after host-side validation and the launch.
+ *   - Errors: every call returns CP_OK (0) or a negative status, checks its
+ *     arguments before launching anything, and launches nothing on error.
+ *     cp_last_error() gives a readable reason for the calling thread's last
+ *     failure.  Device-side contents (e.g. a block-table entry outside the
+ *     cache) are not checked: out-of-range entries are undefined behaviour.
+ */
+#ifndef CP_ATTN_H_
+#define CP_ATTN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CP_OK 0
+#define CP_ERR_INVALID (-1)     /* bad argument (null, range, alignment, shape) */
+#define CP_ERR_UNSUPPORTED (-2) /* well-formed but not built for (e.g. D != 128) */
+#define CP_ERR_HIP (-3)         /* the HIP runtime reported an error */
+#define CP_ERR_CAPACITY (-4)    /* a caller buffer is too small */
+
+#define CP_HEAD_DIM 128
+#define CP_KV_BLOCK_TOKENS 16
+#define CP_MAX_MERGE_PARTS 16
+
+/* kv_rank values of cp_partial_desc besides a rank number 0..C-1. */
+#define CP_KV_ALL (-1)  /* every causally visible suffix key (all-gathered KV) */
+#define CP_KV_NONE (-2) /* no suffix key (prefix-only partial) */
+
+/* Static description of a status code. */
+const char* cp_status_string(int status);
+
+/* Detail of the calling thread's most recent failing call ("" if none). */
+const char* cp_last_error(void);
+
+/* ---------------------------------------------------------------------- */
+/* Shard plan (Sec. 2.1 zigzag, Sec. 2.2 prefix/suffix split) -- host only */
+
+typedef struct cp_chunk {
+  int32_t chunk_id;     /* 0..2C-1 */
+  int32_t reserved;
+  int64_t q_begin;      /* global position of the chunk's first token: P + chunk_id*chunk_len */
+  int64_t q_len;        /* real (unpadded) tokens of the chunk: clamp(R - chunk_id*chunk_len, 0, chunk_len) */
+  int64_t local_offset; /* first local row of the chunk in the rank's buffers */
+} cp_chunk;
+
+typedef struct cp_rank_plan {
+  int32_t C;            /* CP degree */
+  int32_t rank;         /* 0..C-1 */
+  int64_t prefix_len;   /* P: cached tokens, global positions 0..P-1 */
+  int64_t new_len;      /* R: uncached tokens, global positions P..P+R-1 */
+  int64_t padded_len;   /* R rounded up to a multiple of 2C */
+  int64_t chunk_len;    /* padded_len / 2C */
+  int64_t n_rows;       /* chunk[0].q_len + chunk[1].q_len */
+  cp_chunk chunk[2];    /* chunk `rank`, then chunk 2C-1-rank */
+  int64_t visible_pairs;/* per head: sum over rows of (pos + 1), i.e. keys 0..pos */
+} cp_rank_plan;
+
+/*
+ * Plan of rank `rank` of a degree-C worker for a request with P cached and R
+ * uncached tokens (Sec. 2.1, 2.2).  Summed over the C ranks, visible_pairs is
+ * W(R,P) = RP + R(R+1)/2.
+ *   out      host, required; filled on success.
+ *   row_pos  host, optional (NULL): receives the global position of every
+ *            local row, out->n_rows entries; row_pos_cap is its capacity.
+ * Errors: CP_ERR_INVALID if C < 1, rank outside 0..C-1, P < 0, R < 0 or
+ * out == NULL; CP_ERR_CAPACITY if row_pos != NULL and row_pos_cap < n_rows.
+ * R = 0 and R < 2C are legal (empty chunks have q_len = 0).
+ */
+int cp_shard_plan(int64_t prefix_len, int64_t new_len, int32_t C, int32_t rank,
+                  cp_rank_plan* out, int64_t* row_pos, int64_t row_pos_cap);
+
+/*
+ * Restore map (Sec. 2.1): for each suffix index i in 0..R-1, the rank that
+ * holds it and its local row there.  rank_of (int32) and row_of (int64) are
+ * host arrays of capacity `cap` >= R.
+ * Errors: CP_ERR_INVALID for bad P/R/C or NULL arrays; CP_ERR_CAPACITY if cap < R.
+ */
+int cp_shard_inverse(int64_t prefix_len, int64_t new_len, int32_t C,
+                     int32_t* rank_of, int64_t* row_of, int64_t cap);
+
+/* ---------------------------------------------------------------------- */
+/* Partial attention (Sec. 2.1 causal attention of a rank's rows)          */
+
+/*
+ * One unit of partial-attention work: the rows of one rank (plan) against
+ * one set of keys.  Pointers are device memory, 16-byte aligned (lse: 4).
+ *   plan        from cp_shard_plan (checked against (P, R, C, rank)).
+ *   q           bf16 [plan.n_rows][Hq][D]: the rank's query rows, local order.
+ *   k_new,v_new bf16 [R][Hkv][D]: K/V of all R suffix tokens in original
+ *               order (the all-gathered view; suffix index i = position P+i).
+ *               Only rows of the selected suffix keys are read.  May be NULL
+ *               when kv_rank == CP_KV_NONE or R == 0.
+ *   k_cache,v_cache  bf16 [n_blocks][16][Hkv][D]: paged prefix cache.
+ *   block_table int32 [P/16]: physical block of each logical prefix block.
+ *               The three prefix pointers may be NULL unless include_prefix
+ *               and P > 0; then P must be a multiple of 16.
+ *   include_prefix  1: rows attend to all P prefix keys; 0: to none.
+ *   kv_rank     CP_KV_ALL: rows attend to every suffix key at or before them
+ *               (the paper's all-gathered CP); r in 0..C-1: only to the suffix
+ *               keys of rank r's two zigzag chunks (pass-KV partial; the C
+ *               shards partition the suffix); CP_KV_NONE: to no suffix key.
+ *   o           fp32 [plan.n_rows][Hq][D], normalised partial output.
+ *   lse         fp32 [plan.n_rows][Hq], natural-log LSE (-inf: no key).
+ * Merging (cp_attn_merge) the C pass-KV partials plus a prefix-only partial
+ * gives the CP_KV_ALL result with include_prefix = 1.
+ */
+typedef struct cp_partial_desc {
+  cp_rank_plan plan;
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* block_table;
+  int32_t include_prefix;
+  int32_t kv_rank;
+  float* o;
+  float* lse;
+} cp_partial_desc;
+
+/*
+ * Device workspace bytes cp_attn_partial needs for this descriptor set (the
+ * device copy of the descriptors and the scheduled work list).  0 on invalid
+ * arguments (and cp_last_error says why).
+ */
+size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_descs,
+                                      int32_t n_heads_q, int32_t n_heads_kv);
+
+/*
+ * Partial attention of every descriptor, in one kernel launch.
+ *   descs       host array of n_descs descriptors (read during the call only);
+ *               n_descs == 0 is a no-op.  Descriptors may come from different
+ *               requests (ragged lengths); output buffers must not overlap.
+ *   n_heads_q, n_heads_kv  Hq and Hkv, Hq % Hkv == 0.
+ *   head_dim    must be 128 (else CP_ERR_UNSUPPORTED).
+ *   softmax_scale  <= 0 selects 1/sqrt(head_dim) (the paper's 1/sqrt(d_h)).
+ *   workspace   device buffer of workspace_bytes >= the size above; it is
+ *               written by an asynchronous copy on `stream` and read by the
+ *               kernel, so it must not be reused until the stream reaches
+ *               this work.
+ * Each call stages the descriptor copy through pinned host memory owned by
+ * the library (allocated on first use, kept until process exit).
+ * Errors: CP_ERR_INVALID (shapes, plans, pointers, alignment, kv_rank),
+ * CP_ERR_UNSUPPORTED (head_dim), CP_ERR_CAPACITY (workspace), CP_ERR_HIP.
+ */
+int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
+                    int32_t n_heads_kv, int32_t head_dim, float softmax_scale,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* Exact log-sum-exp merge of partials (+ optional restore of order)      */
+
+/*
+ * Merge n_parts partials of the same rows that were computed over disjoint
+ * key sets:  LSE = ln sum_i e^{LSE_i},  O = sum_i e^{LSE_i - LSE} O_i
+ * (partials with LSE_i = -inf weigh 0; all -inf gives O = 0, LSE = -inf).
+ *   o_parts, lse_parts  host arrays of n_parts device pointers (1..16):
+ *               o_parts[i] fp32 [n_tokens][n_heads][D], lse_parts[i] fp32
+ *               [n_tokens][n_heads].  n_parts == 1 copies (and restores).
+ *   o_out       [n_out][n_heads][D], fp32, or bf16 when out_bf16 != 0.
+ *   lse_out     fp32 [n_out][n_heads]; may be NULL.
+ *   restore     host, optional: the plan the rows came from.  NULL: token t
+ *               is written to row t (n_out = n_tokens).  Otherwise local row t
+ *               of that rank is written to its suffix index (position - P),
+ *               the Sec. 2.1 restore, so o_out is [R][n_heads][D] and every
+ *               rank's merge can write into one shared output; n_tokens must
+ *               equal restore->n_rows.
+ * Errors: CP_ERR_INVALID (counts, NULL pointers, alignment, plan mismatch),
+ * CP_ERR_UNSUPPORTED (head_dim != 128), CP_ERR_HIP.
+ */
+int cp_attn_merge(int32_t n_parts, const float* const* o_parts, const float* const* lse_parts,
+                  int64_t n_tokens, int32_t n_heads, int32_t head_dim, void* o_out,
+                  int32_t out_bf16, float* lse_out, const cp_rank_plan* restore, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CP_ATTN_H_ */

@@ -1,0 +1,16 @@
+"""MI355X-native context-parallel prefill attention (arXiv 2609.04774 hot path).
+
+``paper_2609_04774_amd.cpattn`` is the Python binding of libcpattn (the C ABI
+in include/cp_attn.h over hand-written gfx950 HIP kernels);
+``paper_2609_04774_amd.build`` compiles that library in-tree.  The binding is
+imported on first use, so building works before the library exists.
+"""
+
+__all__ = ["cpattn", "build"]
+
+
+def __getattr__(name):
+    if name in ("cpattn", "build"):
+        import importlib
+        return importlib.import_module(f"{__name__}.{name}")
+    raise AttributeError(name)

@@ -1,0 +1,224 @@
+"""ctypes binding of libcpattn (include/cp_attn.h): argument marshalling only.
+
+Every computation happens in the library's host code and HIP kernels; this
+module only turns torch tensors into device pointers, Python ints into C
+integers and non-zero statuses into exceptions.  Importing it fails loudly if
+the library has not been built (``python -m paper_2609_04774_amd.build``).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libcpattn.so")
+
+CP_OK = 0
+CP_ERR_INVALID = -1
+CP_ERR_UNSUPPORTED = -2
+CP_ERR_HIP = -3
+CP_ERR_CAPACITY = -4
+CP_HEAD_DIM = 128
+CP_KV_BLOCK_TOKENS = 16
+CP_MAX_MERGE_PARTS = 16
+CP_KV_ALL = -1
+CP_KV_NONE = -2
+
+EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
+            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_merge")
+
+
+class CpChunk(ctypes.Structure):
+    _fields_ = [("chunk_id", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("q_begin", ctypes.c_int64), ("q_len", ctypes.c_int64),
+                ("local_offset", ctypes.c_int64)]
+
+
+class CpRankPlan(ctypes.Structure):
+    _fields_ = [("C", ctypes.c_int32), ("rank", ctypes.c_int32),
+                ("prefix_len", ctypes.c_int64), ("new_len", ctypes.c_int64),
+                ("padded_len", ctypes.c_int64), ("chunk_len", ctypes.c_int64),
+                ("n_rows", ctypes.c_int64), ("chunk", CpChunk * 2),
+                ("visible_pairs", ctypes.c_int64)]
+
+    def as_dict(self) -> dict:
+        return {
+            "C": self.C, "rank": self.rank, "prefix_len": self.prefix_len,
+            "new_len": self.new_len, "padded_len": self.padded_len,
+            "chunk_len": self.chunk_len, "n_rows": self.n_rows,
+            "chunks": [(c.chunk_id, c.q_begin, c.q_len, c.local_offset) for c in self.chunk],
+            "visible_pairs": self.visible_pairs,
+        }
+
+
+class CpPartialDesc(ctypes.Structure):
+    _fields_ = [("plan", CpRankPlan),
+                ("q", ctypes.c_void_p), ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
+                ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("block_table", ctypes.c_void_p),
+                ("include_prefix", ctypes.c_int32), ("kv_rank", ctypes.c_int32),
+                ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
+
+
+class CpError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{detail} [status {status}]")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_04774_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.cp_status_string.restype = ctypes.c_char_p
+    lib.cp_status_string.argtypes = [ctypes.c_int]
+    lib.cp_last_error.restype = ctypes.c_char_p
+    lib.cp_last_error.argtypes = []
+    lib.cp_shard_plan.restype = ctypes.c_int
+    lib.cp_shard_plan.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.POINTER(CpRankPlan), ctypes.c_void_p, ctypes.c_int64]
+    lib.cp_shard_inverse.restype = ctypes.c_int
+    lib.cp_shard_inverse.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+    lib.cp_attn_partial_workspace_size.restype = ctypes.c_size_t
+    lib.cp_attn_partial_workspace_size.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32,
+                                                   ctypes.c_int32, ctypes.c_int32]
+    lib.cp_attn_partial.restype = ctypes.c_int
+    lib.cp_attn_partial.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
+                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.cp_attn_merge.restype = ctypes.c_int
+    lib.cp_attn_merge.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
+                                  ctypes.POINTER(ctypes.c_void_p), ctypes.c_int64, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                  ctypes.POINTER(CpRankPlan), ctypes.c_void_p]
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != CP_OK:
+        raise CpError(status, lib.cp_last_error().decode() or lib.cp_status_string(status).decode())
+
+
+def status_string(status: int) -> str:
+    return lib.cp_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib.cp_last_error().decode()
+
+
+# --- plan ---------------------------------------------------------------------
+
+def shard_plan(prefix_len: int, new_len: int, C: int, rank: int, with_rows: bool = True):
+    """cp_shard_plan: (CpRankPlan, row_pos as a list of ints or None)."""
+    import numpy as np
+    plan = CpRankPlan()
+    _check(lib.cp_shard_plan(prefix_len, new_len, C, rank, ctypes.byref(plan), None, 0))
+    if not with_rows:
+        return plan, None
+    rows = np.zeros(max(1, plan.n_rows), dtype=np.int64)
+    _check(lib.cp_shard_plan(prefix_len, new_len, C, rank, ctypes.byref(plan),
+                             rows.ctypes.data_as(ctypes.c_void_p), plan.n_rows))
+    return plan, rows[: plan.n_rows]
+
+
+def shard_inverse(prefix_len: int, new_len: int, C: int):
+    """cp_shard_inverse: (rank_of int32[R], row_of int64[R]) as numpy arrays."""
+    import numpy as np
+    rank_of = np.zeros(max(1, new_len), dtype=np.int32)
+    row_of = np.zeros(max(1, new_len), dtype=np.int64)
+    _check(lib.cp_shard_inverse(prefix_len, new_len, C, rank_of.ctypes.data_as(ctypes.c_void_p),
+                                row_of.ctypes.data_as(ctypes.c_void_p), new_len))
+    return rank_of[:new_len], row_of[:new_len]
+
+
+# --- partial attention ----------------------------------------------------------
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=None,
+              block_table=None, include_prefix: bool = True, kv_rank: int = CP_KV_ALL) -> CpPartialDesc:
+    """A cp_partial_desc over torch device tensors (layouts in include/cp_attn.h)."""
+    d = CpPartialDesc()
+    d.plan = plan
+    d.q = _ptr(q)
+    d.k_new = _ptr(k_new)
+    d.v_new = _ptr(v_new)
+    d.k_cache = _ptr(k_cache)
+    d.v_cache = _ptr(v_cache)
+    d.block_table = _ptr(block_table)
+    d.include_prefix = 1 if include_prefix else 0
+    d.kv_rank = kv_rank
+    d.o = _ptr(o)
+    d.lse = _ptr(lse)
+    return d
+
+
+def _desc_array(descs: Sequence[CpPartialDesc]):
+    arr = (CpPartialDesc * max(1, len(descs)))()
+    for i, d in enumerate(descs):
+        arr[i] = d
+    return arr
+
+
+def workspace_size(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int) -> int:
+    arr = _desc_array(descs)
+    n = lib.cp_attn_partial_workspace_size(arr, len(descs), n_heads_q, n_heads_kv)
+    if n == 0 and descs and last_error():
+        raise CpError(CP_ERR_INVALID, last_error())
+    return n
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def attn_partial(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int, workspace,
+                 head_dim: int = CP_HEAD_DIM, softmax_scale: float = 0.0, stream=None,
+                 workspace_bytes: Optional[int] = None):
+    """cp_attn_partial on the given (or current torch) stream.
+
+    ``workspace`` is a torch uint8 device tensor of at least
+    ``workspace_size(descs, ...)`` bytes.
+    """
+    arr = _desc_array(descs)
+    nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
+    _check(lib.cp_attn_partial(arr, len(descs), n_heads_q, n_heads_kv, head_dim,
+                               float(softmax_scale), _ptr(workspace), nbytes,
+                               _stream_handle(stream)))
+
+
+def attn_merge(o_parts, lse_parts, o_out, lse_out=None, restore: Optional[CpRankPlan] = None,
+               n_tokens: Optional[int] = None, n_heads: Optional[int] = None,
+               head_dim: int = CP_HEAD_DIM, stream=None):
+    """cp_attn_merge of torch device tensors; bf16 output when o_out is bf16."""
+    import torch
+    n = len(o_parts)
+    optrs = (ctypes.c_void_p * max(1, n))(*[_ptr(o) for o in o_parts])
+    lptrs = (ctypes.c_void_p * max(1, n))(*[_ptr(s) for s in lse_parts])
+    if n_tokens is None:
+        n_tokens = o_parts[0].shape[0]
+    if n_heads is None:
+        n_heads = o_parts[0].shape[1]
+    out_bf16 = 1 if o_out.dtype == torch.bfloat16 else 0
+    _check(lib.cp_attn_merge(n, optrs, lptrs, n_tokens, n_heads, head_dim, _ptr(o_out), out_bf16,
+                             _ptr(lse_out), ctypes.byref(restore) if restore is not None else None,
+                             _stream_handle(stream)))
+
+
+def default_scale(head_dim: int = CP_HEAD_DIM) -> float:
+    return 1.0 / math.sqrt(head_dim)

@@ -1,0 +1,353 @@
+// Host side of the C ABI: argument checks, the per-launch work list, the
+// staging of descriptors into the caller's workspace, and the launches.
+//
+// Work list.  Every descriptor contributes, per non-empty chunk of its rank,
+// ceil(q_len / q_per_wg) query blocks times (Hkv * groups_per_kv) head
+// groups.  Items are ordered longest first (visible keys per item), which
+// makes the hardware's in-order workgroup dispatch an LPT schedule, and are
+// interleaved so that item i lands on XCD i % 8 with all items of one KV head
+// group on the same XCD: the workgroups streaming one head's K/V share that
+// XCD's L2.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace cpattn;
+
+namespace {
+
+constexpr int kXcds = 8;
+constexpr size_t kItemsAlign = 256;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int gcd_int(int a, int b) {
+  while (b) {
+    int t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+struct Shape {
+  int heads_per_wg, q_per_wg, groups_per_kv;
+};
+
+Shape shape_for(int Hq, int Hkv) {
+  const int G = Hq / Hkv;
+  Shape s;
+  s.heads_per_wg = gcd_int(G, 8);
+  s.q_per_wg = kRowsPerWG / s.heads_per_wg;
+  s.groups_per_kv = G / s.heads_per_wg;
+  return s;
+}
+
+int check_heads(int32_t Hq, int32_t Hkv, const char* who) {
+  if (Hq < 1 || Hkv < 1) return fail(CP_ERR_INVALID, std::string(who) + ": head counts must be >= 1");
+  if (Hq % Hkv) return fail(CP_ERR_INVALID, std::string(who) + ": n_heads_q must be a multiple of n_heads_kv");
+  if (Hq > 4096) return fail(CP_ERR_UNSUPPORTED, std::string(who) + ": more than 4096 query heads");
+  return CP_OK;
+}
+
+// Validates one descriptor and converts it to the kernel's form.
+int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
+  const std::string who = "cp_attn_partial: desc " + std::to_string(idx) + ": ";
+  const cp_rank_plan& pl = x.plan;
+  cp_rank_plan ref;
+  if (make_plan(pl.prefix_len, pl.new_len, pl.C, pl.rank, &ref) != CP_OK)
+    return fail(CP_ERR_INVALID, who + "plan has invalid (P, R, C, rank)");
+  if (!plan_equal(ref, pl)) return fail(CP_ERR_INVALID, who + "plan does not match cp_shard_plan(P, R, C, rank)");
+  if (pl.n_rows > ((int64_t)1 << 31)) return fail(CP_ERR_UNSUPPORTED, who + "more than 2^31 rows");
+  const int64_t P = pl.prefix_len, R = pl.new_len;
+  if (x.kv_rank < CP_KV_NONE || x.kv_rank >= pl.C) return fail(CP_ERR_INVALID, who + "kv_rank out of range");
+  if (x.include_prefix != 0 && x.include_prefix != 1) return fail(CP_ERR_INVALID, who + "include_prefix must be 0 or 1");
+  if (pl.n_rows > 0) {
+    if (!x.q || !x.o || !x.lse) return fail(CP_ERR_INVALID, who + "q, o and lse are required");
+    if (!aligned(x.q, 16) || !aligned(x.o, 16) || !aligned(x.lse, 4))
+      return fail(CP_ERR_INVALID, who + "q/o must be 16-byte and lse 4-byte aligned");
+  }
+  const bool use_suffix = x.kv_rank != CP_KV_NONE && R > 0;
+  if (use_suffix && pl.n_rows > 0) {
+    if (!x.k_new || !x.v_new) return fail(CP_ERR_INVALID, who + "k_new and v_new are required");
+    if (!aligned(x.k_new, 16) || !aligned(x.v_new, 16))
+      return fail(CP_ERR_INVALID, who + "k_new/v_new must be 16-byte aligned");
+  }
+  const bool use_prefix = x.include_prefix && P > 0;
+  if (use_prefix && pl.n_rows > 0) {
+    if (P % CP_KV_BLOCK_TOKENS) return fail(CP_ERR_INVALID, who + "prefix_len must be a multiple of 16 when the prefix is read");
+    if (!x.k_cache || !x.v_cache || !x.block_table)
+      return fail(CP_ERR_INVALID, who + "k_cache, v_cache and block_table are required");
+    if (!aligned(x.k_cache, 16) || !aligned(x.v_cache, 16) || !aligned(x.block_table, 4))
+      return fail(CP_ERR_INVALID, who + "k_cache/v_cache must be 16-byte and block_table 4-byte aligned");
+    if (P > INT32_MAX) return fail(CP_ERR_UNSUPPORTED, who + "prefix beyond 2^31 tokens");
+  }
+  DevDesc d;
+  std::memset(&d, 0, sizeof(d));
+  d.q = static_cast<const uint16_t*>(x.q);
+  d.k_new = static_cast<const uint16_t*>(x.k_new);
+  d.v_new = static_cast<const uint16_t*>(x.v_new);
+  d.k_cache = static_cast<const uint16_t*>(x.k_cache);
+  d.v_cache = static_cast<const uint16_t*>(x.v_cache);
+  d.block_table = x.block_table;
+  d.o = x.o;
+  d.lse = x.lse;
+  d.P = P;
+  d.R = R;
+  for (int i = 0; i < 2; ++i) {
+    d.q_begin[i] = pl.chunk[i].q_begin;
+    d.q_len[i] = pl.chunk[i].q_len;
+    d.local_off[i] = pl.chunk[i].local_offset;
+  }
+  d.prefix_keys = use_prefix ? (int32_t)P : 0;
+  d.n_seg = 0;
+  if (use_suffix) {
+    if (x.kv_rank == CP_KV_ALL) {
+      d.seg_lo[0] = P;
+      d.seg_hi[0] = P + R;
+      d.n_seg = 1;
+    } else {
+      // Rank kv_rank's own suffix keys: its chunks kv_rank and 2C-1-kv_rank.
+      const int64_t s = pl.chunk_len;
+      const int64_t ids[2] = {x.kv_rank, 2 * (int64_t)pl.C - 1 - x.kv_rank};
+      for (int i = 0; i < 2; ++i) {
+        const int64_t lo = ids[i] * s;
+        const int64_t hi = std::min(R, lo + s);
+        if (hi > lo) {
+          d.seg_lo[d.n_seg] = P + lo;
+          d.seg_hi[d.n_seg] = P + hi;
+          ++d.n_seg;
+        }
+      }
+    }
+  }
+  *out = d;
+  return CP_OK;
+}
+
+struct Plan {
+  std::vector<DevDesc> descs;
+  std::vector<WorkItem> items;
+  Shape shape;
+};
+
+int64_t item_keys(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
+  const int64_t last = std::min(qb * q_per_wg + q_per_wg, d.q_len[chunk]) - 1;
+  const int64_t pos_hi = d.q_begin[chunk] + last;
+  int64_t keys = d.prefix_keys;
+  for (int s = 0; s < d.n_seg; ++s) keys += std::max<int64_t>(0, std::min(d.seg_hi[s], pos_hi + 1) - d.seg_lo[s]);
+  return keys;
+}
+
+int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, Plan* out) {
+  int st = check_heads(Hq, Hkv, "cp_attn_partial");
+  if (st != CP_OK) return st;
+  if (n_descs < 0) return fail(CP_ERR_INVALID, "cp_attn_partial: n_descs < 0");
+  if (n_descs > 0 && !descs) return fail(CP_ERR_INVALID, "cp_attn_partial: descs is NULL");
+  out->shape = shape_for(Hq, Hkv);
+  const Shape& sh = out->shape;
+  out->descs.resize(n_descs);
+  for (int i = 0; i < n_descs; ++i) {
+    st = to_dev(descs[i], i, &out->descs[i]);
+    if (st != CP_OK) return st;
+  }
+  const int n_groups = Hkv * sh.groups_per_kv;
+  struct Cand {
+    int64_t cost;
+    WorkItem w;
+  };
+  std::vector<std::vector<Cand>> per_xcd(kXcds);
+  int64_t total = 0;
+  for (int i = 0; i < n_descs; ++i) {
+    const DevDesc& d = out->descs[i];
+    for (int c = 0; c < 2; ++c) {
+      if (d.q_len[c] == 0) continue;
+      const int64_t nqb = (d.q_len[c] + sh.q_per_wg - 1) / sh.q_per_wg;
+      for (int64_t qb = 0; qb < nqb; ++qb) {
+        const int64_t keys = item_keys(d, c, qb, sh.q_per_wg);
+        for (int g = 0; g < n_groups; ++g) {
+          per_xcd[g % kXcds].push_back(Cand{keys, WorkItem{i, c, (int32_t)qb, g}});
+          ++total;
+        }
+      }
+    }
+  }
+  if (total > 0x7fffffffLL) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: work list beyond 2^31 workgroups");
+  for (auto& v : per_xcd)
+    std::stable_sort(v.begin(), v.end(), [](const Cand& a, const Cand& b) { return a.cost > b.cost; });
+  out->items.clear();
+  out->items.reserve((size_t)total);
+  std::vector<size_t> head(kXcds, 0);
+  for (int64_t i = 0; i < total; ++i) {
+    int x = (int)(i % kXcds);
+    if (head[x] == per_xcd[x].size()) {
+      // This XCD's list ran dry: take the costliest remaining item anywhere.
+      int best = -1;
+      for (int y = 0; y < kXcds; ++y)
+        if (head[y] < per_xcd[y].size() && (best < 0 || per_xcd[y][head[y]].cost > per_xcd[best][head[best]].cost))
+          best = y;
+      x = best;
+    }
+    out->items.push_back(per_xcd[x][head[x]++].w);
+  }
+  return CP_OK;
+}
+
+size_t items_offset(size_t n_descs) {
+  return (n_descs * sizeof(DevDesc) + kItemsAlign - 1) / kItemsAlign * kItemsAlign;
+}
+
+// Pinned host staging for the descriptor/work-list upload.  A slot is reused
+// only after the copy that read it has completed (its event).
+struct Slot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  int device = -1;
+  bool pending = false;
+};
+constexpr int kSlots = 8;
+std::mutex g_stage_mu;
+Slot g_slots[kSlots];
+int g_next_slot = 0;
+
+int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_stage_mu);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  Slot& s = g_slots[g_next_slot];
+  g_next_slot = (g_next_slot + 1) % kSlots;
+  if (s.pending) {
+    e = hipEventSynchronize(s.ev);
+    if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
+    s.pending = false;
+  }
+  if (s.ev && s.device != dev) {
+    (void)hipEventDestroy(s.ev);
+    s.ev = nullptr;
+  }
+  if (!s.ev) {
+    e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
+    if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
+    s.device = dev;
+  }
+  if (s.cap < bytes) {
+    if (s.host) (void)hipHostFree(s.host);
+    s.host = nullptr;
+    s.cap = 0;
+    const size_t cap = std::max<size_t>(bytes, 64 * 1024);
+    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipHostMalloc (staging): ") + hipGetErrorString(e));
+    s.cap = cap;
+  }
+  std::memcpy(s.host, src, bytes);
+  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipMemcpyAsync (descriptors): ") + hipGetErrorString(e));
+  e = hipEventRecord(s.ev, stream);
+  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
+  s.pending = true;
+  return CP_OK;
+}
+
+}  // namespace
+
+extern "C" size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_descs,
+                                                 int32_t n_heads_q, int32_t n_heads_kv) {
+  Plan plan;
+  if (build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan) != CP_OK) return 0;
+  clear_error();
+  return items_offset(plan.descs.size()) + plan.items.size() * sizeof(WorkItem);
+}
+
+extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
+                               int32_t n_heads_kv, int32_t head_dim, float softmax_scale, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: head_dim must be 128");
+  if (!(softmax_scale == softmax_scale)) return fail(CP_ERR_INVALID, "cp_attn_partial: softmax_scale is NaN");
+  Plan plan;
+  int st = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
+  if (st != CP_OK) return st;
+  if (plan.items.empty()) {
+    clear_error();
+    return CP_OK;
+  }
+  const size_t off = items_offset(plan.descs.size());
+  const size_t need = off + plan.items.size() * sizeof(WorkItem);
+  if (!workspace) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(need) + " bytes");
+  std::vector<unsigned char> host(need, 0);
+  std::memcpy(host.data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
+  std::memcpy(host.data() + off, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+  st = stage_and_copy(host.data(), need, workspace, (hipStream_t)stream);
+  if (st != CP_OK) return st;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
+  PartialParams p;
+  p.descs = static_cast<const DevDesc*>(workspace);
+  p.items = reinterpret_cast<const WorkItem*>(static_cast<unsigned char*>(workspace) + off);
+  p.n_items = (int32_t)plan.items.size();
+  p.Hq = n_heads_q;
+  p.Hkv = n_heads_kv;
+  p.heads_per_wg = plan.shape.heads_per_wg;
+  p.q_per_wg = plan.shape.q_per_wg;
+  p.groups_per_kv = plan.shape.groups_per_kv;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  st = launch_partial(p, stream);
+  if (st == CP_OK) clear_error();
+  return st;
+}
+
+extern "C" int cp_attn_merge(int32_t n_parts, const float* const* o_parts, const float* const* lse_parts,
+                             int64_t n_tokens, int32_t n_heads, int32_t head_dim, void* o_out, int32_t out_bf16,
+                             float* lse_out, const cp_rank_plan* restore, void* stream) {
+  if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_merge: head_dim must be 128");
+  if (n_parts < 1 || n_parts > CP_MAX_MERGE_PARTS) return fail(CP_ERR_INVALID, "cp_attn_merge: n_parts must be 1..16");
+  if (!o_parts || !lse_parts) return fail(CP_ERR_INVALID, "cp_attn_merge: o_parts/lse_parts is NULL");
+  if (n_tokens < 0 || n_heads < 1) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens < 0 or n_heads < 1");
+  if (out_bf16 != 0 && out_bf16 != 1) return fail(CP_ERR_INVALID, "cp_attn_merge: out_bf16 must be 0 or 1");
+  MergeParams p;
+  std::memset(&p, 0, sizeof(p));
+  if (n_tokens > 0) {
+    for (int i = 0; i < n_parts; ++i) {
+      if (!o_parts[i] || !lse_parts[i]) return fail(CP_ERR_INVALID, "cp_attn_merge: NULL partial pointer");
+      if (!aligned(o_parts[i], 16) || !aligned(lse_parts[i], 4))
+        return fail(CP_ERR_INVALID, "cp_attn_merge: partial O must be 16-byte, LSE 4-byte aligned");
+      p.o[i] = o_parts[i];
+      p.lse[i] = lse_parts[i];
+    }
+    if (!o_out) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out is NULL");
+    if (!aligned(o_out, 16)) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out must be 16-byte aligned");
+    if (lse_out && !aligned(lse_out, 4)) return fail(CP_ERR_INVALID, "cp_attn_merge: lse_out must be 4-byte aligned");
+  }
+  if (restore) {
+    cp_rank_plan ref;
+    if (make_plan(restore->prefix_len, restore->new_len, restore->C, restore->rank, &ref) != CP_OK ||
+        !plan_equal(ref, *restore))
+      return fail(CP_ERR_INVALID, "cp_attn_merge: restore plan does not match cp_shard_plan");
+    if (restore->n_rows != n_tokens) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens != restore->n_rows");
+    p.restore = 1;
+    p.first_len = restore->chunk[0].q_len;
+    p.first_dst = restore->chunk[0].q_begin - restore->prefix_len;
+    p.second_dst = restore->chunk[1].q_begin - restore->prefix_len;
+  }
+  p.n_parts = n_parts;
+  p.n_heads = n_heads;
+  p.n_tokens = n_tokens;
+  p.o_out = o_out;
+  p.lse_out = lse_out;
+  p.out_bf16 = out_bf16;
+  int st = launch_merge(p, stream);
+  if (st == CP_OK) clear_error();
+  return st;
+}

@@ -1,0 +1,99 @@
+// Internal declarations shared by the host ABI code and the HIP kernels of
+// libcpattn.  Not part of the public C ABI (that is include/cp_attn.h).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "cp_attn.h"
+
+namespace cpattn {
+
+// Records a failure reason for cp_last_error() and returns `status`.
+int fail(int status, const std::string& why);
+void clear_error();
+
+// Re-derives a plan from (P, R, C, rank); shared by cp_shard_plan and the
+// descriptor checks of cp_attn_partial / cp_attn_merge.
+int make_plan(int64_t P, int64_t R, int32_t C, int32_t rank, cp_rank_plan* out);
+bool plan_equal(const cp_rank_plan& a, const cp_rank_plan& b);
+
+// ---------------------------------------------------------------------------
+// Partial attention: what one launch consumes.
+
+constexpr int kHeadDim = 128;
+constexpr int kBlockTokens = 16;
+constexpr int kRowsPerWG = 256;      // (query, head) rows per workgroup
+constexpr int kThreads = 256;        // 4 wave64s
+
+// One descriptor as the kernel reads it.  Key sets are expressed as global
+// positions: the prefix [0, prefix_keys) through the block table, then up to
+// two suffix ranges [seg_lo, seg_hi) read from k_new / v_new row (pos - P).
+struct DevDesc {
+  const uint16_t* q;
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const uint16_t* k_cache;
+  const uint16_t* v_cache;
+  const int32_t* block_table;
+  float* o;
+  float* lse;
+  int64_t P;
+  int64_t R;
+  int64_t q_begin[2];
+  int64_t q_len[2];
+  int64_t local_off[2];
+  int64_t seg_lo[2];
+  int64_t seg_hi[2];
+  int32_t n_seg;
+  int32_t prefix_keys;
+  int64_t reserved;
+};
+
+// One workgroup's unit: a block of query positions of one chunk of one
+// descriptor, for one group of query heads sharing a KV head.
+struct WorkItem {
+  int32_t desc;
+  int32_t chunk;
+  int32_t q_block;
+  int32_t head_group;
+};
+
+struct PartialParams {
+  const DevDesc* descs;
+  const WorkItem* items;
+  int32_t n_items;
+  int32_t Hq;
+  int32_t Hkv;
+  int32_t heads_per_wg;   // query heads of one KV head handled by one workgroup
+  int32_t q_per_wg;       // query positions per workgroup (heads_per_wg * q_per_wg = 256)
+  int32_t groups_per_kv;  // (Hq / Hkv) / heads_per_wg
+  float scale_log2;       // softmax scale * log2(e)
+  float scale;            // softmax scale
+};
+
+int launch_partial(const PartialParams& p, void* stream);
+
+// ---------------------------------------------------------------------------
+// LSE merge.
+
+struct MergeParams {
+  const float* o[CP_MAX_MERGE_PARTS];
+  const float* lse[CP_MAX_MERGE_PARTS];
+  int32_t n_parts;
+  int32_t n_heads;
+  int64_t n_tokens;
+  void* o_out;
+  float* lse_out;
+  int32_t out_bf16;
+  int32_t restore;        // 1: map local row t to its suffix index
+  int64_t first_len;      // rows of the rank's first chunk
+  int64_t first_dst;      // suffix index of the first chunk's first row
+  int64_t second_dst;     // suffix index of the second chunk's first row
+};
+
+int launch_merge(const MergeParams& p, void* stream);
+
+}  // namespace cpattn

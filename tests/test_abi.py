@@ -1,0 +1,217 @@
+"""C-ABI checks that need no GPU: exports, plan parity, argument errors.
+
+Every error case here fails host-side validation, which runs before any HIP
+call, so nothing touches a device.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import plan as oplan
+from paper_2609_04774_amd import cpattn as cp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cp_attn.h")
+
+
+def _declared_functions():
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cp_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    declared = _declared_functions()
+    assert set(declared) == set(cp.EXPORTED)
+    for name in declared:
+        assert hasattr(cp.lib, name), name
+
+
+def test_status_strings():
+    for st in (cp.CP_OK, cp.CP_ERR_INVALID, cp.CP_ERR_UNSUPPORTED, cp.CP_ERR_HIP, cp.CP_ERR_CAPACITY):
+        assert cp.status_string(st) and cp.status_string(st) != "unknown status"
+    assert cp.status_string(12345) == "unknown status"
+
+
+def test_struct_layout_matches_header():
+    # 4+4 + 5*8 + 2*(4+4+3*8) + 8 bytes
+    assert ctypes.sizeof(cp.CpChunk) == 32
+    assert ctypes.sizeof(cp.CpRankPlan) == 8 + 5 * 8 + 2 * 32 + 8
+    assert ctypes.sizeof(cp.CpPartialDesc) == ctypes.sizeof(cp.CpRankPlan) + 6 * 8 + 8 + 2 * 8
+
+
+PLAN_SWEEP = [(P, R, C) for P in (0, 16, 48, 49152) for R in (0, 1, 3, 7, 16, 100, 1024, 1000)
+              for C in (1, 2, 3, 4, 8)]
+
+
+@pytest.mark.parametrize("P,R,C", PLAN_SWEEP)
+def test_plan_bit_exact_vs_oracle(P, R, C):
+    for r in range(C):
+        got, rows = cp.shard_plan(P, R, C, r)
+        ref = oplan.shard_plan_fast(P, R, C, r) if R > 64 else oplan.shard_plan(P, R, C, r)
+        d = got.as_dict()
+        for key in ("C", "rank", "prefix_len", "new_len", "padded_len", "chunk_len", "n_rows",
+                    "visible_pairs"):
+            assert d[key] == ref[key], key
+        assert [tuple(c) for c in d["chunks"]] == [tuple(c) for c in ref["chunks"]]
+        assert rows.tolist() == ref["row_pos"]
+
+
+@pytest.mark.parametrize("P,R,C", [(0, 32768, 4), (49152, 16384, 2), (0, 131072, 8), (0, 1024, 2)])
+def test_plan_full_size_configs(P, R, C):
+    total = 0
+    for r in range(C):
+        got, rows = cp.shard_plan(P, R, C, r)
+        ref = oplan.shard_plan_fast(P, R, C, r)
+        assert got.visible_pairs == ref["visible_pairs"]
+        assert rows.tolist() == ref["row_pos"]
+        total += got.visible_pairs
+    assert total == oplan.remaining_workload(R, P)
+
+
+@pytest.mark.parametrize("P,R,C", [(0, 1024, 2), (16, 37, 8), (0, 3, 4), (32, 100, 3), (0, 0, 2)])
+def test_inverse_bit_exact_vs_oracle(P, R, C):
+    rank_of, row_of = cp.shard_inverse(P, R, C)
+    ref_rank, ref_row = oplan.inverse_map(P, R, C)
+    assert rank_of.tolist() == ref_rank
+    assert row_of.tolist() == ref_row
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_plan_errors():
+    plan = cp.CpRankPlan()
+    assert cp.lib.cp_shard_plan(0, 10, 0, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert "C must be" in cp.last_error()
+    assert cp.lib.cp_shard_plan(0, 10, 2, 2, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(0, 10, 2, -1, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(-1, 10, 2, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(0, -1, 2, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(0, 10, 2, 0, None, None, 0) == cp.CP_ERR_INVALID
+    rows = np.zeros(2, dtype=np.int64)
+    assert cp.lib.cp_shard_plan(0, 10, 2, 0, ctypes.byref(plan),
+                                rows.ctypes.data_as(ctypes.c_void_p), 2) == cp.CP_ERR_CAPACITY
+    a = np.zeros(4, dtype=np.int32)
+    b = np.zeros(4, dtype=np.int64)
+    assert cp.lib.cp_shard_inverse(0, 10, 2, a.ctypes.data_as(ctypes.c_void_p),
+                                   b.ctypes.data_as(ctypes.c_void_p), 4) == cp.CP_ERR_CAPACITY
+    assert cp.lib.cp_shard_inverse(0, 10, 2, None, None, 10) == cp.CP_ERR_INVALID
+    # A successful call clears the error detail.
+    assert cp.lib.cp_shard_plan(0, 10, 2, 0, ctypes.byref(plan), None, 0) == cp.CP_OK
+    assert cp.last_error() == ""
+
+
+FAKE = 1 << 20          # aligned addresses that are never dereferenced
+
+
+def _desc(P=0, R=64, C=2, rank=0, **kw):
+    plan, _ = cp.shard_plan(P, R, C, rank, with_rows=False)
+    d = cp.CpPartialDesc()
+    d.plan = plan
+    d.q = kw.get("q", FAKE)
+    d.k_new = kw.get("k_new", FAKE * 2)
+    d.v_new = kw.get("v_new", FAKE * 3)
+    d.k_cache = kw.get("k_cache", FAKE * 4)
+    d.v_cache = kw.get("v_cache", FAKE * 5)
+    d.block_table = kw.get("block_table", FAKE * 6)
+    d.include_prefix = kw.get("include_prefix", 1)
+    d.kv_rank = kw.get("kv_rank", cp.CP_KV_ALL)
+    d.o = kw.get("o", FAKE * 7)
+    d.lse = kw.get("lse", FAKE * 8)
+    return d
+
+
+def _partial_status(descs, Hq=8, Hkv=2, D=128, ws=FAKE * 16, ws_bytes=1 << 30):
+    arr = (cp.CpPartialDesc * max(1, len(descs)))(*descs)
+    return cp.lib.cp_attn_partial(arr, len(descs), Hq, Hkv, D, 0.0, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("case,kw,args,status", [
+    ("head_dim 64", {}, {"D": 64}, cp.CP_ERR_UNSUPPORTED),
+    ("Hq not multiple of Hkv", {}, {"Hq": 6, "Hkv": 4}, cp.CP_ERR_INVALID),
+    ("zero heads", {}, {"Hq": 0}, cp.CP_ERR_INVALID),
+    ("kv_rank >= C", {"kv_rank": 2}, {}, cp.CP_ERR_INVALID),
+    ("kv_rank < -2", {"kv_rank": -3}, {}, cp.CP_ERR_INVALID),
+    ("prefix not block multiple", {"P": 40}, {}, cp.CP_ERR_INVALID),
+    ("null q", {"q": None}, {}, cp.CP_ERR_INVALID),
+    ("null o", {"o": None}, {}, cp.CP_ERR_INVALID),
+    ("null k_new", {"k_new": None}, {}, cp.CP_ERR_INVALID),
+    ("null block table with prefix", {"P": 32, "block_table": None}, {}, cp.CP_ERR_INVALID),
+    ("misaligned q", {"q": FAKE + 2}, {}, cp.CP_ERR_INVALID),
+    ("misaligned k_cache", {"P": 32, "k_cache": FAKE + 8}, {}, cp.CP_ERR_INVALID),
+    ("include_prefix 2", {"include_prefix": 2}, {}, cp.CP_ERR_INVALID),
+    ("workspace too small", {}, {"ws_bytes": 16}, cp.CP_ERR_CAPACITY),
+    ("workspace null", {}, {"ws": None}, cp.CP_ERR_INVALID),
+    ("workspace misaligned", {}, {"ws": FAKE + 64}, cp.CP_ERR_INVALID),
+])
+def test_partial_argument_errors(case, kw, args, status):
+    P = kw.pop("P", 0)
+    d = _desc(P=P, **kw)
+    assert _partial_status([d], **args) == status, case
+    assert cp.last_error() != ""
+
+
+def test_partial_rejects_a_tampered_plan():
+    d = _desc()
+    d.plan.n_rows += 1
+    assert _partial_status([d]) == cp.CP_ERR_INVALID
+    d = _desc()
+    d.plan.chunk[1].q_begin += 1
+    assert _partial_status([d]) == cp.CP_ERR_INVALID
+
+
+def test_partial_prefix_pointers_optional_when_unused():
+    # Prefix not read: the cache pointers may be NULL; the call then fails only
+    # on the (deliberately tiny) workspace, i.e. after every descriptor check.
+    d = _desc(P=40, include_prefix=0, k_cache=None, v_cache=None, block_table=None)
+    assert _partial_status([d], ws_bytes=16) == cp.CP_ERR_CAPACITY
+    d = _desc(kv_rank=cp.CP_KV_NONE, k_new=None, v_new=None, include_prefix=0)
+    assert _partial_status([d], ws_bytes=16) == cp.CP_ERR_CAPACITY
+
+
+def test_partial_empty_work_is_a_no_op():
+    assert _partial_status([]) == cp.CP_OK
+    # A rank with no rows (R < 2C) launches nothing either.
+    d = _desc(R=3, C=4, rank=3, q=None, o=None, lse=None)
+    assert d.plan.n_rows == 0
+    assert _partial_status([d], ws=None, ws_bytes=0) == cp.CP_OK
+
+
+def test_workspace_size_grows_with_work():
+    small = cp.workspace_size([_desc(R=64)], 8, 2)
+    big = cp.workspace_size([_desc(R=4096)], 8, 2)
+    assert 0 < small < big
+    bad = _desc(kv_rank=5)
+    with pytest.raises(cp.CpError):
+        cp.workspace_size([bad], 8, 2)
+
+
+def _merge_status(n_parts=2, n_tokens=4, H=2, D=128, out=FAKE, lse_out=FAKE * 2, restore=None,
+                  parts=None, out_bf16=0):
+    o = (ctypes.c_void_p * max(1, n_parts))(*([FAKE * 3] * n_parts if parts is None else parts))
+    l = (ctypes.c_void_p * max(1, n_parts))(*([FAKE * 4] * n_parts))
+    return cp.lib.cp_attn_merge(n_parts, o, l, n_tokens, H, D, out, out_bf16, lse_out,
+                                ctypes.byref(restore) if restore is not None else None, None)
+
+
+def test_merge_argument_errors():
+    assert _merge_status(n_parts=0) == cp.CP_ERR_INVALID
+    assert _merge_status(n_parts=17) == cp.CP_ERR_INVALID
+    assert _merge_status(D=64) == cp.CP_ERR_UNSUPPORTED
+    assert _merge_status(H=0) == cp.CP_ERR_INVALID
+    assert _merge_status(n_tokens=-1) == cp.CP_ERR_INVALID
+    assert _merge_status(out=None) == cp.CP_ERR_INVALID
+    assert _merge_status(out=FAKE + 4) == cp.CP_ERR_INVALID
+    assert _merge_status(parts=[FAKE * 3, None]) == cp.CP_ERR_INVALID
+    assert _merge_status(out_bf16=3) == cp.CP_ERR_INVALID
+    plan, _ = cp.shard_plan(0, 10, 2, 0, with_rows=False)
+    assert _merge_status(n_tokens=5, restore=plan) == cp.CP_ERR_INVALID   # n_rows is 4
+    plan.chunk[0].q_len = 2
+    assert _merge_status(n_tokens=4, restore=plan) == cp.CP_ERR_INVALID   # tampered plan

@@ -1,0 +1,180 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Small cases compare every output element; the full-size workloads compare
+seeded samples of rows (all heads) that the oracle computes one by one, and
+check properties that hold at any size.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as oatt
+from oracle import plan as oplan
+from paper_2609_04774_amd import cpattn as cp
+
+import gpu_cases as gc
+from gpu_cases import Problem, compare, f64, DEV
+
+pytestmark = pytest.mark.gpu
+
+
+def _restore_all_ranks(prob, kv_mode="allgather"):
+    """Every rank's partial(s), merged and restored into original order by
+    cp_attn_merge; returns (O [R, Hq, D], LSE [R, Hq]) on the GPU."""
+    R, Hq = prob.R, prob.Hq
+    O = torch.full((R, Hq, 128), float("nan"), dtype=torch.float32, device=DEV)
+    LSE = torch.full((R, Hq), float("nan"), dtype=torch.float32, device=DEV)
+    for r in range(prob.C):
+        if kv_mode == "allgather":
+            o, lse, plan, _ = prob.gpu_rank(r)
+            parts = [(o, lse)]
+        else:
+            parts = []
+            if prob.P:
+                o, lse, plan, _ = prob.gpu_rank(r, kv_rank=cp.CP_KV_NONE, include_prefix=True)
+                parts.append((o, lse))
+            for s in range(prob.C):
+                o, lse, plan, _ = prob.gpu_rank(r, kv_rank=s, include_prefix=False)
+                parts.append((o, lse))
+        if plan.n_rows == 0:
+            continue
+        cp.attn_merge([p[0] for p in parts], [p[1] for p in parts], O, LSE, restore=plan)
+    torch.cuda.synchronize()
+    return O, LSE
+
+
+def _oracle_full(prob):
+    d = prob.np()
+    if prob.P:
+        kp = oatt.gather_paged(d["kc"], d["bt"], prob.P)
+        vp = oatt.gather_paged(d["vc"], d["bt"], prob.P)
+        k = np.concatenate([kp, d["k"]])
+        v = np.concatenate([vp, d["v"]])
+        q = np.concatenate([np.zeros((prob.P,) + d["q"].shape[1:]), d["q"]])
+        O, L = oatt.full_causal_attention(q, k, v)
+        return O[prob.P:], L[prob.P:]
+    return oatt.full_causal_attention(d["q"], d["k"], d["v"])
+
+
+def test_tiny_workload_both_ranks_restored():
+    """1024 tokens, C=2, 8/2 heads, N(0,1)/sqrt(128): both ranks, restored."""
+    w = synth.WORKLOADS["tiny_1k_c2"]
+    prob = Problem(w.L, w.P, w.C, w.Hq, w.Hkv, w.seed, data_scale=w.data_scale)
+    O, L = _restore_all_ranks(prob)
+    Or, Lr = _oracle_full(prob)
+    compare(f64(O), f64(L), Or, Lr, "tiny allgather restore")
+
+
+def test_tiny_workload_pass_kv_partials_merged():
+    w = synth.WORKLOADS["tiny_1k_c2"]
+    prob = Problem(w.L, w.P, w.C, w.Hq, w.Hkv, w.seed, data_scale=w.data_scale)
+    O, L = _restore_all_ranks(prob, kv_mode="passkv")
+    Or, Lr = _oracle_full(prob)
+    compare(f64(O), f64(L), Or, Lr, "tiny pass-KV merge")
+
+
+# (L, P, C, Hq, Hkv, data_scale, q_scale, seed): ragged suffixes, R < 2C,
+# GQA ratios 1/2/4/8/16, prefixes that are not tile multiples, unscaled and
+# peaky logits.
+SHAPES = [
+    (1000, 0, 2, 8, 2, 1.0, 1.0, 11),
+    (777, 0, 4, 4, 4, 1.0, 1.0, 12),
+    (5, 0, 4, 8, 1, 1.0, 1.0, 13),
+    (300, 48, 2, 32, 8, 1.0, 1.0, 14),
+    (700, 208, 8, 16, 2, 1.0, 8.0, 15),
+    (513, 0, 1, 8, 8, 1.0, 1.0, 16),
+    (640, 80, 3, 16, 1, 1.0, 1.0, 17),
+    (400, 16, 2, 24, 8, 1.0, 1.0, 18),
+    (1025, 0, 2, 64, 8, 1.0, 1.0, 19),
+    (333, 0, 2, 6, 2, 1.0 / math.sqrt(128.0), 1.0, 20),
+]
+
+
+@pytest.mark.parametrize("L,P,C,Hq,Hkv,ds,qs,seed", SHAPES)
+def test_every_rank_matches_oracle(L, P, C, Hq, Hkv, ds, qs, seed):
+    prob = Problem(L, P, C, Hq, Hkv, seed, data_scale=ds, q_scale=qs)
+    for r in range(C):
+        o, lse, plan, rows = prob.gpu_rank(r)
+        ref = oplan.shard_plan_fast(P, L - P, C, r)
+        assert rows.tolist() == ref["row_pos"]
+        Or, Lr = prob.oracle_rank(r)
+        compare(f64(o), f64(lse), Or, Lr, f"rank {r}")
+
+
+@pytest.mark.parametrize("L,P,C,Hq,Hkv,seed", [(1000, 0, 2, 8, 2, 21), (600, 96, 4, 8, 2, 22),
+                                                (131, 32, 8, 4, 1, 23)])
+def test_pass_kv_and_prefix_only_partials(L, P, C, Hq, Hkv, seed):
+    """Each kv_rank shard (some rows see nothing: LSE = -inf, O = 0) and the
+    prefix-only partial match the oracle element by element."""
+    prob = Problem(L, P, C, Hq, Hkv, seed)
+    for r in range(C):
+        for s in range(C):
+            o, lse, _, _ = prob.gpu_rank(r, kv_rank=s, include_prefix=(s == 0))
+            Or, Lr = prob.oracle_rank(r, kv_rank=s, include_prefix=(s == 0))
+            compare(f64(o), f64(lse), Or, Lr, f"rank {r} shard {s}")
+        if P:
+            o, lse, _, _ = prob.gpu_rank(r, kv_rank=cp.CP_KV_NONE, include_prefix=True)
+            Or, Lr = prob.oracle_rank(r, kv_rank=cp.CP_KV_NONE, include_prefix=True)
+            compare(f64(o), f64(lse), Or, Lr, f"rank {r} prefix only")
+
+
+def test_explicit_softmax_scale():
+    prob = Problem(300, 0, 2, 8, 2, 31)
+    o, lse, _, _ = prob.gpu_rank(0, scale=0.05)
+    Or, Lr = prob.oracle_rank(0, scale=0.05)
+    compare(f64(o), f64(lse), Or, Lr, "scale 0.05")
+
+
+def test_merge_kernel_matches_oracle_merge():
+    g = torch.Generator().manual_seed(41)
+    n_tok, H = 300, 6
+    for n in (1, 2, 3, 8, 16):
+        outs = [torch.randn(n_tok, H, 128, generator=g) for _ in range(n)]
+        lses = [torch.randn(n_tok, H, generator=g) * 4 for _ in range(n)]
+        # Some partials carry no keys, and a few rows carry none anywhere.
+        for i in range(0, n, 2):
+            mask = torch.rand(n_tok, H, generator=g) < 0.3
+            lses[i][mask] = -math.inf
+            outs[i][mask] = 0.0
+        for i in range(n):
+            lses[i][:5] = -math.inf
+            outs[i][:5] = 0.0
+        Or, Lr = oatt.lse_merge([o.double().numpy() for o in outs], [s.double().numpy() for s in lses])
+        od = [o.to(DEV) for o in outs]
+        ld = [s.to(DEV) for s in lses]
+        O = torch.empty(n_tok, H, 128, device=DEV)
+        L = torch.empty(n_tok, H, device=DEV)
+        cp.attn_merge(od, ld, O, L)
+        Ob = torch.empty(n_tok, H, 128, dtype=torch.bfloat16, device=DEV)
+        cp.attn_merge(od, ld, Ob, None)
+        torch.cuda.synchronize()
+        compare(f64(O), f64(L), Or, Lr, f"merge n={n}")
+        # bf16 output: within half an ulp of bf16 at |O| (plus the fp32 error).
+        ob = f64(Ob)
+        assert np.all(np.abs(ob - Or) <= np.abs(Or) * 2.0 ** -8 + 1e-5)
+
+
+def test_results_are_deterministic():
+    prob = Problem(2000, 32, 2, 32, 8, 51)
+    o1, l1, _, _ = prob.gpu_rank(1)
+    o2, l2, _, _ = prob.gpu_rank(1)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_empty_and_degenerate_launches():
+    # R = 0: every rank is empty; the call is a no-op.
+    plan, _ = cp.shard_plan(0, 0, 2, 0)
+    o, lse = gc.alloc_out(1, 8)
+    desc = cp.make_desc(plan, o, None, None, o, lse)
+    gc.run_partials([desc], 8, 2)
+    assert torch.isnan(o).all()
+    # One token: it sees exactly itself, so O = v_0 and LSE = q.k/sqrt(D).
+    prob = Problem(1, 0, 1, 4, 2, 61)
+    o, lse, _, _ = prob.gpu_rank(0)
+    Or, Lr = prob.oracle_rank(0)
+    compare(f64(o), f64(lse), Or, Lr, "single token")
+    assert torch.equal(o[0, 0].cpu(), prob.v[0, 0].float())
