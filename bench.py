@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Benchmark of one CP rank's prefill-attention hot path on one MI355X.
+
+A step is one pass of the whole path for rank 0 of the workload:
+  1. the zigzag shard plan (host, cp_shard_plan);
+  2. partial attention of the rank's rows against each of the C ranks' KV
+     shards (and the paged prefix, if any) -- one cp_attn_partial launch with
+     C (+1) descriptors;
+  3. the exact LSE merge of those partials, writing each row back to its
+     place in the original sequence order (cp_attn_merge with the plan).
+Inputs are resident in HBM before the timed region starts.
+
+value  = 4 * D * Hq * visible_pairs / step time  (TFLOP/s; the two MFMA
+         contractions per visible query-key pair, no credit for masked work).
+roofline = the partial-attention kernel: the same FLOPs / its average launch
+         duration from HIP events on its stream, against 2.5 PFLOP/s dense bf16.
+cpu_baseline = the fp64 oracle on a bounded sample of the same rows.
+
+Usage: python bench.py [--steps K] [--warmup W] [--workload NAME] [--mode passkv|allgather]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+METRIC = "CP-shard causal prefill attention TFLOP/s + % bf16 MFMA peak; merge GB/s"
+DEFAULT_WORKLOAD = "llama3_8b_32k_c4"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--rank", type=int, default=0)
+    ap.add_argument("--mode", choices=["passkv", "allgather"], default="passkv")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="wall-clock budget of the CPU oracle sample (0 disables it)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build executes every CP rank's shard "
+              "on a single MI355X and has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2609_04774_amd import cpattn as cp
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = synth.WORKLOADS[args.workload]
+    P, R, C, Hq, Hkv, D = w.P, w.R, w.C, w.Hq, w.Hkv, w.D
+    rank = args.rank
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    # --- inputs, resident in HBM -------------------------------------------
+    plan, rows = cp.shard_plan(P, R, C, rank)
+    n_rows = plan.n_rows
+    gen = synth.generator(w.seed + 100 * rank, device="cuda")
+    q = synth.randn_bf16(gen, (n_rows, Hq, D), w.data_scale, device="cuda")
+    k = synth.randn_bf16(gen, (R, Hkv, D), w.data_scale, device="cuda")
+    v = synth.randn_bf16(gen, (R, Hkv, D), w.data_scale, device="cuda")
+    prefix = synth.paged_prefix(gen, P, Hkv, D, w.data_scale, spare_blocks=64, device="cuda") if P else None
+    kc = prefix.k_cache if prefix else None
+    vc = prefix.v_cache if prefix else None
+    bt = prefix.block_table if prefix else None
+
+    if args.mode == "passkv":
+        shard_ids = list(range(C))
+        n_parts = C + (1 if P else 0)
+    else:
+        shard_ids = [cp.CP_KV_ALL]
+        n_parts = 1
+    o_parts = torch.empty((n_parts, n_rows, Hq, D), dtype=torch.float32, device=dev)
+    l_parts = torch.empty((n_parts, n_rows, Hq), dtype=torch.float32, device=dev)
+    out = torch.empty((R, Hq, D), dtype=torch.float32, device=dev)
+    out_lse = torch.empty((R, Hq), dtype=torch.float32, device=dev)
+
+    def make_descs(pl):
+        descs = []
+        i = 0
+        if args.mode == "passkv" and P:
+            descs.append(cp.make_desc(pl, q, k, v, o_parts[i], l_parts[i], kc, vc, bt,
+                                      include_prefix=True, kv_rank=cp.CP_KV_NONE))
+            i += 1
+        for s in shard_ids:
+            descs.append(cp.make_desc(pl, q, k, v, o_parts[i], l_parts[i], kc, vc, bt,
+                                      include_prefix=(args.mode == "allgather"), kv_rank=s))
+            i += 1
+        return descs
+
+    ws = torch.empty(max(256, cp.workspace_size(make_descs(plan), Hq, Hkv)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    flop = 4.0 * D * Hq * plan.visible_pairs
+
+    ev = []
+
+    def step(record):
+        pl, _ = cp.shard_plan(P, R, C, rank, with_rows=False)
+        descs = make_descs(pl)
+        e0 = e1 = e2 = None
+        if record:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e2 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
+        if record:
+            e1.record(stream)
+        cp.attn_merge([o_parts[i] for i in range(n_parts)], [l_parts[i] for i in range(n_parts)],
+                      out, out_lse, restore=pl, stream=stream)
+        if record:
+            e2.record(stream)
+            ev.append((e0, e1, e2))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    attn_ms = sum(a.elapsed_time(b) for a, b, _ in ev) / len(ev)
+    merge_ms = sum(b.elapsed_time(c) for _, b, c in ev) / len(ev)
+
+    rows_merged = n_rows * Hq
+    merge_bytes = (n_parts * rows_merged + rows_merged) * (4 * D + 4)
+    merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
+    attn_tflops = flop / (attn_ms * 1e-3) / 1e12
+    value = flop / (ms_step * 1e-3) / 1e12
+
+    # --- CPU oracle on a bounded sample of the same rows ----------------------
+    cpu = None
+    parity = None
+    if args.cpu_seconds > 0:
+        cpu, parity = cpu_baseline(args, w, plan, rows, q, k, v, prefix, out, out_lse, flop)
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "L": w.L, "P": P, "R": R, "C": C, "rank": rank, "Hq": Hq,
+            "Hkv": Hkv, "D": D, "rows": n_rows, "visible_pairs_per_head": plan.visible_pairs,
+            "flop_per_step": flop, "mode": ("pass-KV partials + LSE merge + restore" if args.mode == "passkv"
+                                            else "all-gathered KV partial + restore"),
+            "partials": n_parts,
+        },
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "roofline": {
+            "kernel": "attn_partial_kernel",
+            "bound": "mfma",
+            "achieved": round(attn_tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "launch_ms": round(attn_ms, 4),
+        },
+        "merge": {
+            "kernel": "lse_merge_kernel", "bound": "hbm", "ms": round(merge_ms, 4),
+            "bytes": merge_bytes, "GB_s": round(merge_gbs, 1),
+            "frac": round(merge_gbs / PEAK_HBM_GBS, 4),
+        },
+        "cpu_baseline": cpu,
+        "parity_sample": parity,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(args, w, plan, rows, q, k, v, prefix, out, out_lse, flop_total):
+    """Time the oracle (as it stands) on seeded rows of the same shard, and
+    compare those rows with the GPU's merged output on the way."""
+    import numpy as np
+    import torch
+
+    from oracle import attention as oatt
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    P, R, Hq, D = w.P, w.R, w.Hq, w.D
+    kk = k.cpu().double().numpy()
+    vv = v.cpu().double().numpy()
+    if prefix is not None:
+        bt = prefix.block_table.cpu().numpy().astype(np.int64)
+        kc = prefix.k_cache.cpu().double().numpy()
+        vc = prefix.v_cache.cpu().double().numpy()
+    else:
+        bt = kc = vc = None
+    rng = np.random.default_rng(w.seed)
+    order = rng.permutation(plan.n_rows)
+    # Always include both chunks' first and last rows.
+    c0 = plan.chunk[0].q_len
+    firsts = [0, max(0, c0 - 1), c0, plan.n_rows - 1]
+    order = list(dict.fromkeys([i for i in firsts if 0 <= i < plan.n_rows] + list(order)))
+    done_rows, pairs, err_o, err_l = [], 0, 0.0, 0.0
+    t0 = time.perf_counter()
+    batch = 2
+    while order and time.perf_counter() - t0 < args.cpu_seconds:
+        take, order = order[:batch], order[batch:]
+        idx = np.array(take, dtype=np.int64)
+        pos = rows[idx]
+        qq = q[torch.as_tensor(idx, device=q.device)].cpu().double().numpy()
+        O, L = oatt.rank_partial(qq, pos, P, kk, vv, kc, vc, bt)
+        pairs += int(np.sum(pos + 1))
+        done_rows.extend(take)
+        g_o = out[torch.as_tensor(pos - P, device=out.device)].cpu().double().numpy()
+        g_l = out_lse[torch.as_tensor(pos - P, device=out.device)].cpu().double().numpy()
+        err_o = max(err_o, float(np.max(np.abs(g_o - O))))
+        err_l = max(err_l, float(np.max(np.abs(g_l - L))))
+    elapsed = time.perf_counter() - t0
+    flop = 4.0 * D * Hq * pairs
+    cpu = {
+        "value": round(flop / elapsed / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{len(done_rows)} of {plan.n_rows} rank-{plan.rank} rows x {Hq} heads over all their "
+                  f"visible keys (fp64 numpy), {elapsed:.1f} s",
+        "seconds": round(elapsed, 2),
+        "est_full_step_s": round(flop_total / (flop / elapsed), 1) if flop else None,
+    }
+    parity = {"rows": len(done_rows), "max_abs_o": err_o, "max_abs_lse": err_l,
+              "ok": bool(err_o <= 1e-2 and err_l <= 1e-3)}
+    return cpu, parity
+
+
+if __name__ == "__main__":
+    main()
