@@ -72,6 +72,10 @@ class CpError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_04774_amd.build`")
+    # torch ships its own HIP runtime (same soname).  Loading torch first makes
+    # libcpattn bind to that already-loaded runtime, so the process has one
+    # HIP runtime and torch's streams and allocations are valid in the library.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     lib.cp_status_string.restype = ctypes.c_char_p
     lib.cp_status_string.argtypes = [ctypes.c_int]

@@ -37,9 +37,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTileKeys = 64;
+constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 constexpr int kRowBytes = kHeadDim * 2;
 constexpr int kTileBytes = kTileKeys * kRowBytes;
 
@@ -52,22 +54,125 @@ __device__ __forceinline__ s16x4 ds_read_tr16(const unsigned char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
 
-__global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(PartialParams p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * kTileBytes];
-  unsigned char* const sk = smem;
-  unsigned char* const sv = smem + kTileBytes;
+// Key ranges of one work item: the paged prefix (if read) and up to two
+// suffix ranges, each clipped to the workgroup's last query position.  At
+// most three; selected by a wave-uniform index.
+struct Ranges {
+  int64_t lo[3], hi[3], vis[3];
+  int paged0;  // range 0 is the paged prefix
+  int n;
+};
 
-  const WorkItem it = p.items[blockIdx.x];
-  const DevDesc& d = p.descs[it.desc];
+struct Cursor {
+  int r;       // range index
+  int64_t t0;  // first key position of the tile
+};
+
+__device__ __forceinline__ int64_t sel3(const int64_t (&a)[3], int i) { return i == 0 ? a[0] : (i == 1 ? a[1] : a[2]); }
+
+__device__ __forceinline__ void advance(Cursor& c, const Ranges& rg) {
+  c.t0 += kTileKeys;
+  if (c.t0 >= sel3(rg.vis, c.r)) {
+    ++c.r;
+    c.t0 = sel3(rg.lo, c.r);
+  }
+}
+
+// One global_load_lds_dwordx4: lane l's 16 bytes at `gaddr` land at LDS
+// byte m0 + 16*l.  Issued as inline assembly so the compiler does not treat
+// every later LDS read as depending on it (it cannot tell the two buffers
+// apart); the kernel waits for these loads itself (vmcnt) before the barrier
+// that publishes a tile.
+__device__ __forceinline__ void dma16(const void* gaddr, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t" ::"s"(lds_base),
+      "v"(gaddr)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) unsigned char*)p);
+}
+
+// Issues this wave's share of one K/V tile straight into LDS.  Wave w fills
+// tile rows 16w..16w+15; lane l of load i carries row 16w + 4i + l/16,
+// physical chunk l%16, i.e. logical chunk (l%16) ^ swz(row).  Rows past the
+// visible end read a clamped, in-range row; those keys are masked in the
+// scores.
+__device__ __forceinline__ void issue_tile(const Cursor& c, const Ranges& rg, const DevDesc& d, int kvh,
+                                           int Hkv, int wave, int lane, uint32_t sk, uint32_t sv) {
+  const int64_t vis = sel3(rg.vis, c.r);
+  const bool paged = (c.r == 0) && rg.paged0;
+  const uint16_t* kb = paged ? d.k_cache : d.k_new;
+  const uint16_t* vb = paged ? d.v_cache : d.v_new;
+  int64_t blk = 0;
+  if (paged) {
+    // Prefix tiles start at multiples of 64 keys, so wave w's 16 rows are
+    // exactly logical cache block t0/16 + w (clamped to the last block).
+    int64_t lb = (c.t0 >> 4) + wave;
+    const int64_t last = ((vis + kBlockTokens - 1) >> 4) - 1;
+    lb = lb < last ? lb : last;
+    blk = __builtin_amdgcn_readfirstlane(((const __attribute__((address_space(1))) int32_t*)d.block_table)[lb]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wave * 16 + 4 * i + (lane >> 4);
+    const int chunk = (lane & 15) ^ swz(row);
+    int64_t ridx;
+    if (paged) {
+      ridx = (blk * kBlockTokens + 4 * i + (lane >> 4)) * Hkv + kvh;
+    } else {
+      int64_t pos = c.t0 + row;
+      pos = pos < vis ? pos : vis - 1;
+      ridx = (pos - d.P) * Hkv + kvh;
+    }
+    const int64_t off = ridx * kHeadDim + chunk * 8;
+    const uint32_t lrow = (uint32_t)((wave * 16 + 4 * i) * kRowBytes);
+    dma16(kb + off, sk + lrow);
+    dma16(vb + off, sv + lrow);
+  }
+}
+
+__device__ __forceinline__ float xmax32(float x) {
+  // Max with the lane 32 apart (the other half of the same query's keys).
+  auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                            false, false);
+  return __builtin_fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+}
+
+__device__ __forceinline__ float xsum32(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                            false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+// Running max is only moved when it grows by more than 2^8 in the exponent
+// (per wave); until then probabilities are taken against the stale max and
+// stay below 256, which bf16 and the fp32 sums hold exactly as well.
+constexpr float kLazyRescaleLog2 = 8.f;
+
+// s_waitcnt immediate for vmcnt(0) with expcnt/lgkmcnt left at their maxima
+// (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt_hi[15:14]).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+__global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
+                                                                   const WorkItem* __restrict__ items,
+                                                                   PartialParams p) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[4 * kTileBytes];
+
+  const WorkItem it = items[blockIdx.x];
+  const DevDesc& d = descs[it.desc];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5;
   const int l32 = lane & 31;
 
-  const int64_t q_begin = d.q_begin[it.chunk];
-  const int64_t q_len = d.q_len[it.chunk];
-  const int64_t loff = d.local_off[it.chunk];
+  const int64_t q_begin = it.chunk ? d.q_begin[1] : d.q_begin[0];
+  const int64_t q_len = it.chunk ? d.q_len[1] : d.q_len[0];
+  const int64_t loff = it.chunk ? d.local_off[1] : d.local_off[0];
   const int Hq = p.Hq;
   const int Hkv = p.Hkv;
   const int kvh = it.head_group / p.groups_per_kv;
@@ -98,21 +203,68 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(PartialParams
   }
   const bool wave_active = wave_hi >= 0;
 
+  // Key ranges and the number of 64-key tiles over all of them.
+  Ranges rg;
+  rg.n = 0;
+  rg.paged0 = 0;
+  int n_tiles = 0;
+#pragma unroll
+  for (int i = 0; i < 3; ++i) rg.lo[i] = rg.hi[i] = rg.vis[i] = 0;
+  if (d.prefix_keys > 0) {
+    rg.lo[0] = 0;
+    rg.hi[0] = rg.vis[0] = d.prefix_keys;
+    rg.paged0 = 1;
+    rg.n = 1;
+    n_tiles += (int)((d.prefix_keys + kTileKeys - 1) / kTileKeys);
+  }
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if (s < d.n_seg) {
+      const int64_t lo = s ? d.seg_lo[1] : d.seg_lo[0];
+      const int64_t hi = s ? d.seg_hi[1] : d.seg_hi[0];
+      const int64_t vis = hi < wg_pos_hi + 1 ? hi : wg_pos_hi + 1;
+      if (vis > lo) {
+        if (rg.n == 0) {
+          rg.lo[0] = lo; rg.hi[0] = hi; rg.vis[0] = vis;
+        } else if (rg.n == 1) {
+          rg.lo[1] = lo; rg.hi[1] = hi; rg.vis[1] = vis;
+        } else {
+          rg.lo[2] = lo; rg.hi[2] = hi; rg.vis[2] = vis;
+        }
+        ++rg.n;
+        n_tiles += (int)((vis - lo + kTileKeys - 1) / kTileKeys);
+      }
+    }
+  }
+
+  Cursor cc{0, rg.lo[0]};
+  Cursor lc = cc;
+  const uint32_t lds0 = lds_addr(smem);
+  if (n_tiles > 0) issue_tile(lc, rg, d, kvh, Hkv, wave, lane, lds0, lds0 + kTileBytes);
+
   // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
   // head-dim values of its query, for each of the 8 steps of 16 along D.
   bf16x8 qf[2][8];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
-    const uint16_t* qrow = d.q + ((loff + qidx_b[b]) * Hq + head_b[b]) * kHeadDim + half * 8;
+    const __attribute__((address_space(1))) bf16x8* qrow =
+        (const __attribute__((address_space(1))) bf16x8*)(d.q + ((loff + qidx_b[b]) * Hq + head_b[b]) * kHeadDim +
+                                                          half * 8);
 #pragma unroll
     for (int ds = 0; ds < 8; ++ds) {
       if (valid_b[b]) {
-        qf[b][ds] = *reinterpret_cast<const bf16x8*>(qrow + ds * 16);
+        qf[b][ds] = qrow[2 * ds];
       } else {
         qf[b][ds] = bf16x8{};
       }
     }
   }
+
+  // Query fragments and tile 0 have landed.  Waiting here, with the
+  // builtin the compiler's own wait-count tracking sees, keeps it from
+  // re-waiting on the query loads inside the loop, where vmcnt also counts
+  // the next tile's in-flight loads.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
   f32x16 o[4][2];
 #pragma unroll
@@ -120,140 +272,128 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(PartialParams
 #pragma unroll
     for (int b = 0; b < 2; ++b) o[db][b] = f32x16{};
   float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  float l_run[2] = {0.f, 0.f};   // sum of fp32 probabilities (for the LSE)
+  float lb_run[2] = {0.f, 0.f};  // sum of their bf16 roundings (normalises O)
   const float sl2 = p.scale_log2;
 
-  for (int seg = 0; seg <= d.n_seg; ++seg) {
-    int64_t lo, hi;
-    const bool paged = (seg == 0);
-    if (paged) {
-      lo = 0;
-      hi = d.prefix_keys;
-    } else {
-      lo = d.seg_lo[seg - 1];
-      hi = d.seg_hi[seg - 1];
+  for (int j = 0; j < n_tiles; ++j) {
+    // This wave's loads of tile j are done; after the barrier every wave's
+    // are, and every wave has finished reading the buffer tile j+1 reuses.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    unsigned char* const sk = smem + (j & 1) * 2 * kTileBytes;
+    unsigned char* const sv = sk + kTileBytes;
+    if (j + 1 < n_tiles) {
+      advance(lc, rg);
+      const uint32_t nk = lds0 + ((j + 1) & 1) * 2 * kTileBytes;
+      issue_tile(lc, rg, d, kvh, Hkv, wave, lane, nk, nk + kTileBytes);
     }
-    const int64_t hi_vis = (hi < wg_pos_hi + 1) ? hi : wg_pos_hi + 1;
-    const uint16_t* kbase = paged ? d.k_cache : d.k_new;
-    const uint16_t* vbase = paged ? d.v_cache : d.v_new;
-    for (int64_t t0 = lo; t0 < hi_vis; t0 += kTileKeys) {
-      // Stage K and V tiles: 64 keys x 16 chunks of 16 bytes each; zero rows
-      // past the visible end so no memory outside the key range is read.
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int idx = tid + kThreads * i;
-        const int key = idx >> 4;
-        const int c = idx & 15;
-        const int64_t pos = t0 + key;
-        u32x4 kv = u32x4{0u, 0u, 0u, 0u};
-        u32x4 vv = u32x4{0u, 0u, 0u, 0u};
-        if (pos < hi_vis) {
-          int64_t row;
-          if (paged) {
-            const int64_t blk = d.block_table[pos >> 4];
-            row = (blk * kBlockTokens + (pos & (kBlockTokens - 1))) * Hkv + kvh;
-          } else {
-            row = (pos - d.P) * Hkv + kvh;
-          }
-          kv = *reinterpret_cast<const u32x4*>(kbase + row * kHeadDim + c * 8);
-          vv = *reinterpret_cast<const u32x4*>(vbase + row * kHeadDim + c * 8);
-        }
-        *reinterpret_cast<u32x4*>(sk + lds_off(key, c)) = kv;
-        *reinterpret_cast<u32x4*>(sv + lds_off(key, c)) = vv;
-      }
-      __syncthreads();
+    const int64_t t0 = cc.t0;
+    const int64_t hi = sel3(rg.hi, cc.r);
+    advance(cc, rg);
 
-      if (wave_active && t0 <= wave_hi) {
-        const bool need_mask = (t0 + kTileKeys > hi) || (t0 + kTileKeys - 1 > wave_lo);
-        f32x16 s[2][2];
+    if (wave_active && t0 <= wave_hi) {
+      const bool need_mask = (t0 + kTileKeys > hi) || (t0 + kTileKeys - 1 > wave_lo);
+      f32x16 s[2][2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) s[kb][b] = f32x16{};
+#pragma unroll
+      for (int ds = 0; ds < 8; ++ds) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + lds_off(kb * 32 + l32, 2 * ds + half));
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+            s[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[b][ds], s[kb][b], 0, 0, 0);
+        }
+      }
+      if (need_mask) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) s[kb][b] = f32x16{};
-#pragma unroll
-        for (int ds = 0; ds < 8; ++ds) {
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) {
-            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + lds_off(kb * 32 + l32, 2 * ds + half));
+          for (int r = 0; r < 16; ++r) {
+            const int64_t kp = t0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
 #pragma unroll
             for (int b = 0; b < 2; ++b)
-              s[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[b][ds], s[kb][b], 0, 0, 0);
+              if (kp >= hi || kp > pos_b[b]) s[kb][b][r] = -INFINITY;
           }
-        }
-        if (need_mask) {
+      }
+      // Online softmax per query column; the two lane halves hold disjoint
+      // keys of the same query and always agree on the running max.
+      bf16x8 pf[2][4];
 #pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
+      for (int b = 0; b < 2; ++b) {
+        float mx = s[0][b][0];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int64_t kp = t0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-              for (int b = 0; b < 2; ++b)
-                if (kp >= hi || kp > pos_b[b]) s[kb][b][r] = -INFINITY;
-            }
-        }
-        // Online softmax per query column; the two lane halves hold disjoint
-        // keys of the same query and agree on the running max.
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          float mx = -INFINITY;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][b][r]);
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          const float m_new = fmaxf(m_run[b], mx);
-          const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-          const float alpha = __builtin_amdgcn_exp2f((m_run[b] - m_use) * sl2);
-          m_run[b] = m_new;
-          const float neg = -m_use * sl2;
-          float rs = 0.f;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][b][r], sl2, neg));
-              s[kb][b][r] = e;
-              rs += e;
-            }
-          l_run[b] = l_run[b] * alpha + rs;
+          for (int r = 0; r < 16; ++r) mx = __builtin_fmaxf(mx, s[kb][b][r]);
+        mx = xmax32(mx);
+        const float m_new = __builtin_fmaxf(m_run[b], mx);
+        const bool grow = (m_new - m_run[b]) * sl2 > kLazyRescaleLog2;
+        if (__any(grow)) {
+          const float m_upd = grow ? m_new : m_run[b];
+          const float alpha = __builtin_amdgcn_exp2f((m_run[b] - m_upd) * sl2);
+          m_run[b] = m_upd;
+          l_run[b] *= alpha;
+          lb_run[b] *= alpha;
 #pragma unroll
           for (int db = 0; db < 4; ++db) o[db][b] *= alpha;
         }
-        // P^T fragments: k-step ks covers keys 16ks..16ks+15 of the tile; slot
-        // t of lane half h is key 16ks + (t/4)*8 + 4h + t%4, which is exactly
-        // accumulator register 8*(ks%2) + t of key block ks/2.
-        bf16x8 pf[2][4];
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-            for (int t = 0; t < 8; ++t) pf[b][ks][t] = (__bf16)s[ks >> 1][b][8 * (ks & 1) + t];
-        // O^T += V^T P^T.  The transposed read gives lane (group g, index i)
-        // the four keys kbase..kbase+3 of column d0 + i, where the group's 16
-        // lanes read rows kbase + i/4 at columns d0 + 4*(i%4).
-        const int grp = lane >> 4;
-        const int gi = lane & 15;
+        const float neg = (m_run[b] == -INFINITY) ? 0.f : -m_run[b] * sl2;
+        // Probabilities are rounded to bf16 once for the PV product.  Two row
+        // sums: the fp32 one gives the LSE; the sum of the rounded values
+        // (v_dot2 against (1, 1)) normalises O, so that O's numerator and
+        // denominator use the same weights (exact for a single dominant key).
+        float rs = 0.f;
+        float rsb = 0.f;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          const int row1 = ks * 16 + half * 4 + (gi >> 2);
-          const int row2 = row1 + 8;
+          bf16x2 pp[4];
 #pragma unroll
-          for (int db = 0; db < 4; ++db) {
-            const int dcol = db * 32 + (grp & 1) * 16 + 4 * (gi & 3);
-            const int c = dcol >> 3;
-            const int e = (dcol & 7) * 2;
-            const s16x4 lo4 = ds_read_tr16(sv + row1 * kRowBytes + ((c ^ swz(row1)) << 4) + e);
-            const s16x4 hi4 = ds_read_tr16(sv + row2 * kRowBytes + ((c ^ swz(row2)) << 4) + e);
-            const s16x8 v8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
-            const bf16x8 vf = __builtin_bit_cast(bf16x8, v8);
-#pragma unroll
-            for (int b = 0; b < 2; ++b)
-              o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
+          for (int t = 0; t < 4; ++t) {
+            const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks >> 1][b][8 * (ks & 1) + 2 * t], sl2, neg));
+            const float e1 =
+                __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks >> 1][b][8 * (ks & 1) + 2 * t + 1], sl2, neg));
+            pp[t] = bf16x2{(__bf16)e0, (__bf16)e1};
+            rs += e0 + e1;
+            rsb = __builtin_amdgcn_fdot2_f32_bf16(pp[t], kOnes, rsb, false);
           }
+          // P^T fragment for k-step ks (keys 16ks..16ks+15 of the tile): slot
+          // t of lane half h is key 16ks + (t/4)*8 + 4h + t%4, which is
+          // exactly accumulator register 8*(ks%2) + t of key block ks/2.
+          pf[b][ks] = __builtin_shufflevector(__builtin_shufflevector(pp[0], pp[1], 0, 1, 2, 3),
+                                              __builtin_shufflevector(pp[2], pp[3], 0, 1, 2, 3), 0, 1, 2, 3, 4, 5,
+                                              6, 7);
+        }
+        l_run[b] += rs;
+        lb_run[b] += rsb;
+      }
+      // O^T += V^T P^T.  The transposed read gives lane (group g, index i)
+      // the four keys kbase..kbase+3 of column d0 + i, where the group's 16
+      // lanes read rows kbase + i/4 at columns d0 + 4*(i%4).
+      const int grp = lane >> 4;
+      const int gi = lane & 15;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int row1 = ks * 16 + half * 4 + (gi >> 2);
+        const int row2 = row1 + 8;
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const int dcol = db * 32 + (grp & 1) * 16 + 4 * (gi & 3);
+          const int c = dcol >> 3;
+          const int e = (dcol & 7) * 2;
+          const s16x4 lo4 = ds_read_tr16(sv + row1 * kRowBytes + ((c ^ swz(row1)) << 4) + e);
+          const s16x4 hi4 = ds_read_tr16(sv + row2 * kRowBytes + ((c ^ swz(row2)) << 4) + e);
+          const s16x8 v8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, v8);
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+            o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
         }
       }
-      __syncthreads();
     }
   }
 
@@ -261,9 +401,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(PartialParams
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
-    const float lt = l_run[b] + __shfl_xor(l_run[b], 32);
-    const bool live = (m_run[b] != -INFINITY) && (lt > 0.f);
-    const float inv = live ? 1.f / lt : 0.f;
+    const float lt = xsum32(l_run[b]);
+    const float ltb = xsum32(lb_run[b]);
+    const bool live = (m_run[b] != -INFINITY) && (lt > 0.f) && (ltb > 0.f);
+    const float inv = live ? 1.f / ltb : 0.f;
     if (valid_b[b]) {
       float* orow = d.o + ((loff + qidx_b[b]) * Hq + head_b[b]) * kHeadDim;
 #pragma unroll
@@ -286,7 +427,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(PartialParams
 
 int launch_partial(const PartialParams& p, void* stream) {
   if (p.n_items == 0) return CP_OK;
-  hipLaunchKernelGGL(attn_partial_kernel, dim3((unsigned)p.n_items), dim3(kThreads), 0, (hipStream_t)stream, p);
+  hipLaunchKernelGGL(attn_partial_kernel, dim3((unsigned)p.n_items), dim3(kThreads), 0, (hipStream_t)stream,
+                     p.descs, p.items, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial launch: ") + hipGetErrorString(e));
   return CP_OK;
