@@ -97,39 +97,41 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
 }
 
 // Issues this wave's share of one K/V tile straight into LDS.  Wave w fills
-// tile rows 16w..16w+15; lane l of load i carries row 16w + 4i + l/16,
-// physical chunk l%16, i.e. logical chunk (l%16) ^ swz(row).  Rows past the
-// visible end read a clamped, in-range row; those keys are masked in the
-// scores.
+// tile rows RPW*w .. RPW*w + RPW-1; lane l of load i carries row
+// RPW*w + 4i + l/16, physical chunk l%16, i.e. logical chunk (l%16) ^ swz(row).
+// Rows past the visible end read a clamped, in-range row; those keys are
+// masked in the scores.
+template <int RPW>
 __device__ __forceinline__ void issue_tile(const Cursor& c, const Ranges& rg, const DevDesc& d, int kvh,
                                            int Hkv, int wave, int lane, uint32_t sk, uint32_t sv) {
   const int64_t vis = sel3(rg.vis, c.r);
   const bool paged = (c.r == 0) && rg.paged0;
   const uint16_t* kb = paged ? d.k_cache : d.k_new;
   const uint16_t* vb = paged ? d.v_cache : d.v_new;
+  const int row0 = wave * RPW;
   int64_t blk = 0;
   if (paged) {
-    // Prefix tiles start at multiples of 64 keys, so wave w's 16 rows are
-    // exactly logical cache block t0/16 + w (clamped to the last block).
-    int64_t lb = (c.t0 >> 4) + wave;
+    // Prefix tiles start at multiples of 64 keys, so this wave's rows lie in
+    // logical cache block t0/16 + row0/16 (clamped to the last block).
+    int64_t lb = (c.t0 >> 4) + (row0 >> 4);
     const int64_t last = ((vis + kBlockTokens - 1) >> 4) - 1;
     lb = lb < last ? lb : last;
     blk = __builtin_amdgcn_readfirstlane(((const __attribute__((address_space(1))) int32_t*)d.block_table)[lb]);
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = wave * 16 + 4 * i + (lane >> 4);
+  for (int i = 0; i < RPW / 4; ++i) {
+    const int row = row0 + 4 * i + (lane >> 4);
     const int chunk = (lane & 15) ^ swz(row);
     int64_t ridx;
     if (paged) {
-      ridx = (blk * kBlockTokens + 4 * i + (lane >> 4)) * Hkv + kvh;
+      ridx = (blk * kBlockTokens + (row & (kBlockTokens - 1))) * Hkv + kvh;
     } else {
       int64_t pos = c.t0 + row;
       pos = pos < vis ? pos : vis - 1;
       ridx = (pos - d.P) * Hkv + kvh;
     }
     const int64_t off = ridx * kHeadDim + chunk * 8;
-    const uint32_t lrow = (uint32_t)((wave * 16 + 4 * i) * kRowBytes);
+    const uint32_t lrow = (uint32_t)((row0 + 4 * i) * kRowBytes);
     dma16(kb + off, sk + lrow);
     dma16(vb + off, sv + lrow);
   }
@@ -157,9 +159,13 @@ constexpr float kLazyRescaleLog2 = 8.f;
 // (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt_hi[15:14]).
 constexpr int kWaitVmcnt0 = 0x0F70;
 
-__global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
-                                                                   const WorkItem* __restrict__ items,
-                                                                   PartialParams p) {
+// NB = blocks of 32 rows per wave; 8/NB waves cover the workgroup's 256 rows.
+template <int NB>
+__global__ __launch_bounds__(64 * (8 / NB), 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
+                                                                        const WorkItem* __restrict__ items,
+                                                                        PartialParams p) {
+  constexpr int kWaves = 8 / NB;
+  constexpr int kRPW = kTileKeys / kWaves;  // tile rows each wave loads
   __shared__ __attribute__((aligned(1024))) unsigned char smem[4 * kTileBytes];
 
   const WorkItem it = items[blockIdx.x];
@@ -182,14 +188,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
   const int64_t wg_last = (qb0 + p.q_per_wg < q_len ? qb0 + p.q_per_wg : q_len) - 1;
   const int64_t wg_pos_hi = q_begin + wg_last;
 
-  int head_b[2];
-  int64_t qidx_b[2];
-  int64_t pos_b[2];
-  bool valid_b[2];
+  int head_b[NB];
+  int64_t qidx_b[NB];
+  int64_t pos_b[NB];
+  bool valid_b[NB];
   int64_t wave_lo = INT64_MAX, wave_hi = -1;
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int bi = 2 * wave + b;
+  for (int b = 0; b < NB; ++b) {
+    const int bi = NB * wave + b;
     head_b[b] = head0 + bi / qblocks_per_head;
     const int qo = (bi % qblocks_per_head) * 32;
     qidx_b[b] = qb0 + qo + l32;
@@ -240,13 +246,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
   Cursor cc{0, rg.lo[0]};
   Cursor lc = cc;
   const uint32_t lds0 = lds_addr(smem);
-  if (n_tiles > 0) issue_tile(lc, rg, d, kvh, Hkv, wave, lane, lds0, lds0 + kTileBytes);
+  if (n_tiles > 0) issue_tile<kRPW>(lc, rg, d, kvh, Hkv, wave, lane, lds0, lds0 + kTileBytes);
 
   // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
   // head-dim values of its query, for each of the 8 steps of 16 along D.
-  bf16x8 qf[2][8];
+  bf16x8 qf[NB][8];
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < NB; ++b) {
     const __attribute__((address_space(1))) bf16x8* qrow =
         (const __attribute__((address_space(1))) bf16x8*)(d.q + ((loff + qidx_b[b]) * Hq + head_b[b]) * kHeadDim +
                                                           half * 8);
@@ -266,14 +272,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
   // the next tile's in-flight loads.
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
-  f32x16 o[4][2];
+  f32x16 o[4][NB];
+  float m_run[NB], l_run[NB], lb_run[NB];  // running max; sums of fp32 / bf16-rounded probabilities
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int b = 0; b < NB; ++b) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b) o[db][b] = f32x16{};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};   // sum of fp32 probabilities (for the LSE)
-  float lb_run[2] = {0.f, 0.f};  // sum of their bf16 roundings (normalises O)
+    for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
+    m_run[b] = -INFINITY;
+    l_run[b] = 0.f;
+    lb_run[b] = 0.f;
+  }
   const float sl2 = p.scale_log2;
 
   for (int j = 0; j < n_tiles; ++j) {
@@ -286,7 +294,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
     if (j + 1 < n_tiles) {
       advance(lc, rg);
       const uint32_t nk = lds0 + ((j + 1) & 1) * 2 * kTileBytes;
-      issue_tile(lc, rg, d, kvh, Hkv, wave, lane, nk, nk + kTileBytes);
+      issue_tile<kRPW>(lc, rg, d, kvh, Hkv, wave, lane, nk, nk + kTileBytes);
     }
     const int64_t t0 = cc.t0;
     const int64_t hi = sel3(rg.hi, cc.r);
@@ -294,18 +302,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
 
     if (wave_active && t0 <= wave_hi) {
       const bool need_mask = (t0 + kTileKeys > hi) || (t0 + kTileKeys - 1 > wave_lo);
-      f32x16 s[2][2];
+      f32x16 s[2][NB];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) s[kb][b] = f32x16{};
+        for (int b = 0; b < NB; ++b) s[kb][b] = f32x16{};
 #pragma unroll
       for (int ds = 0; ds < 8; ++ds) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + lds_off(kb * 32 + l32, 2 * ds + half));
 #pragma unroll
-          for (int b = 0; b < 2; ++b)
+          for (int b = 0; b < NB; ++b)
             s[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[b][ds], s[kb][b], 0, 0, 0);
         }
       }
@@ -316,15 +324,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
           for (int r = 0; r < 16; ++r) {
             const int64_t kp = t0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
+            for (int b = 0; b < NB; ++b)
               if (kp >= hi || kp > pos_b[b]) s[kb][b][r] = -INFINITY;
           }
       }
       // Online softmax per query column; the two lane halves hold disjoint
       // keys of the same query and always agree on the running max.
-      bf16x8 pf[2][4];
+      bf16x8 pf[NB][4];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < NB; ++b) {
         float mx = s[0][b][0];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -390,7 +398,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
           const s16x8 v8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
           const bf16x8 vf = __builtin_bit_cast(bf16x8, v8);
 #pragma unroll
-          for (int b = 0; b < 2; ++b)
+          for (int b = 0; b < NB; ++b)
             o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
         }
       }
@@ -400,7 +408,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < NB; ++b) {
     const float lt = xsum32(l_run[b]);
     const float ltb = xsum32(lb_run[b]);
     const bool live = (m_run[b] != -INFINITY) && (lt > 0.f) && (ltb > 0.f);
@@ -427,8 +435,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_partial_kernel(const DevDesc
 
 int launch_partial(const PartialParams& p, void* stream) {
   if (p.n_items == 0) return CP_OK;
-  hipLaunchKernelGGL(attn_partial_kernel, dim3((unsigned)p.n_items), dim3(kThreads), 0, (hipStream_t)stream,
-                     p.descs, p.items, p);
+  if (p.waves_per_wg == 4) {
+    hipLaunchKernelGGL(attn_partial_kernel<2>, dim3((unsigned)p.n_items), dim3(256), 0, (hipStream_t)stream,
+                       p.descs, p.items, p);
+  } else {
+    hipLaunchKernelGGL(attn_partial_kernel<1>, dim3((unsigned)p.n_items), dim3(512), 0, (hipStream_t)stream,
+                       p.descs, p.items, p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial launch: ") + hipGetErrorString(e));
   return CP_OK;

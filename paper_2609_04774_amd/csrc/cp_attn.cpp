@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <numeric>
@@ -303,6 +304,8 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
   p.groups_per_kv = plan.shape.groups_per_kv;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.waves_per_wg = 8;
+  if (const char* w = std::getenv("CPATTN_WAVES")) p.waves_per_wg = (std::atoi(w) == 4) ? 4 : 8;
   st = launch_partial(p, stream);
   if (st == CP_OK) clear_error();
   return st;

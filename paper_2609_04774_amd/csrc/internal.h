@@ -26,7 +26,6 @@ bool plan_equal(const cp_rank_plan& a, const cp_rank_plan& b);
 constexpr int kHeadDim = 128;
 constexpr int kBlockTokens = 16;
 constexpr int kRowsPerWG = 256;      // (query, head) rows per workgroup
-constexpr int kThreads = 256;        // 4 wave64s
 
 // One descriptor as the kernel reads it.  Key sets are expressed as global
 // positions: the prefix [0, prefix_keys) through the block table, then up to
@@ -72,6 +71,7 @@ struct PartialParams {
   int32_t groups_per_kv;  // (Hq / Hkv) / heads_per_wg
   float scale_log2;       // softmax scale * log2(e)
   float scale;            // softmax scale
+  int32_t waves_per_wg;   // 4 (two 32-row blocks per wave) or 8 (one block per wave)
 };
 
 int launch_partial(const PartialParams& p, void* stream);
