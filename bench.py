@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--mode", choices=["passkv", "allgather"], default="passkv")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="before timing, run one plain device copy of this many MiB, so that a "
+                         "counter profile of the run can scale FETCH_SIZE/WRITE_SIZE by a known size")
     return ap.parse_args()
 
 
@@ -110,6 +113,13 @@ def main():
         return descs
 
     ws = torch.empty(max(256, cp.workspace_size(make_descs(plan), Hq, Hkv)), dtype=torch.uint8, device=dev)
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     stream = torch.cuda.current_stream()
     flop = 4.0 * D * Hq * plan.visible_pairs
 

@@ -305,7 +305,6 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.waves_per_wg = 8;
-  if (const char* w = std::getenv("CPATTN_WAVES")) p.waves_per_wg = (std::atoi(w) == 4) ? 4 : 8;
   st = launch_partial(p, stream);
   if (st == CP_OK) clear_error();
   return st;
