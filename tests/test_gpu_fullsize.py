@@ -1,0 +1,184 @@
+"""GPU parity at the full workload sizes, in the launch configuration that
+bench.py times: one cp_attn_partial launch with the rank's C pass-KV partials
+(plus a prefix-only partial when a prefix is cached), then cp_attn_merge with
+the rank's plan, which writes every row to its place in the original order.
+
+The oracle recomputes seeded samples of rows (every head) one by one: the
+first and last rows of each chunk, rows on both sides of 64- and 256-row
+boundaries, and random rows.  Properties that hold at any size are checked
+on every row: the merged pass-KV result equals the all-gathered partial, no
+NaN anywhere, and every restored row is written exactly once.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as oatt
+from oracle import plan as oplan
+from paper_2609_04774_amd import cpattn as cp
+
+from gpu_cases import DEV, LSE_TOL, O_TOL, compare, f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(w, rank):
+    """Rank `rank`'s queries plus the whole suffix K/V (and paged prefix),
+    drawn on the GPU from the workload's seed."""
+    g = synth.generator(w.seed + 100 * rank, device="cuda")
+    plan, rows = cp.shard_plan(w.P, w.R, w.C, rank)
+    q = synth.randn_bf16(g, (plan.n_rows, w.Hq, w.D), w.data_scale, device="cuda")
+    k = synth.randn_bf16(g, (w.R, w.Hkv, w.D), w.data_scale, device="cuda")
+    v = synth.randn_bf16(g, (w.R, w.Hkv, w.D), w.data_scale, device="cuda")
+    pre = synth.paged_prefix(g, w.P, w.Hkv, w.D, w.data_scale, spare_blocks=64, device="cuda") if w.P else None
+    return plan, rows, q, k, v, pre
+
+
+def _run_passkv(w, plan, q, k, v, pre):
+    """The bench's step: pass-KV partials (+ prefix partial) and the merge."""
+    n_parts = w.C + (1 if w.P else 0)
+    o = torch.empty((n_parts, plan.n_rows, w.Hq, w.D), dtype=torch.float32, device=DEV)
+    l = torch.empty((n_parts, plan.n_rows, w.Hq), dtype=torch.float32, device=DEV)
+    kc, vc, bt = (pre.k_cache, pre.v_cache, pre.block_table) if pre else (None, None, None)
+    descs = []
+    i = 0
+    if w.P:
+        descs.append(cp.make_desc(plan, q, k, v, o[i], l[i], kc, vc, bt, include_prefix=True,
+                                  kv_rank=cp.CP_KV_NONE))
+        i += 1
+    for s in range(w.C):
+        descs.append(cp.make_desc(plan, q, k, v, o[i], l[i], kc, vc, bt, include_prefix=False, kv_rank=s))
+        i += 1
+    ws = torch.empty(max(256, cp.workspace_size(descs, w.Hq, w.Hkv)), dtype=torch.uint8, device=DEV)
+    cp.attn_partial(descs, w.Hq, w.Hkv, ws)
+    out = torch.full((w.R, w.Hq, w.D), float("nan"), dtype=torch.float32, device=DEV)
+    out_lse = torch.full((w.R, w.Hq), float("nan"), dtype=torch.float32, device=DEV)
+    cp.attn_merge([o[j] for j in range(n_parts)], [l[j] for j in range(n_parts)], out, out_lse, restore=plan)
+    torch.cuda.synchronize()
+    return out, out_lse
+
+
+def _run_allgather(w, plan, q, k, v, pre):
+    o = torch.empty((plan.n_rows, w.Hq, w.D), dtype=torch.float32, device=DEV)
+    l = torch.empty((plan.n_rows, w.Hq), dtype=torch.float32, device=DEV)
+    kc, vc, bt = (pre.k_cache, pre.v_cache, pre.block_table) if pre else (None, None, None)
+    d = cp.make_desc(plan, q, k, v, o, l, kc, vc, bt, include_prefix=True, kv_rank=cp.CP_KV_ALL)
+    ws = torch.empty(max(256, cp.workspace_size([d], w.Hq, w.Hkv)), dtype=torch.uint8, device=DEV)
+    cp.attn_partial([d], w.Hq, w.Hkv, ws)
+    torch.cuda.synchronize()
+    return o, l
+
+
+def _sample_rows(plan, n_random, seed):
+    rng = np.random.default_rng(seed)
+    picks = set()
+    for c in plan.chunk:
+        lo, n = c.local_offset, c.q_len
+        if n == 0:
+            continue
+        for r in (0, 1, 63, 64, 255, 256, n - 2, n - 1):
+            if 0 <= r < n:
+                picks.add(lo + r)
+    picks.update(int(x) for x in rng.choice(plan.n_rows, size=min(n_random, plan.n_rows), replace=False))
+    return np.array(sorted(picks), dtype=np.int64)
+
+
+def _check_workload(name, rank, n_random):
+    w = synth.WORKLOADS[name]
+    plan, rows, q, k, v, pre = _inputs(w, rank)
+    ref_plan = oplan.shard_plan_fast(w.P, w.R, w.C, rank)
+    assert rows.tolist() == ref_plan["row_pos"], "C-ABI plan differs from the oracle's"
+    out, out_lse = _run_passkv(w, plan, q, k, v, pre)
+    # Every restored row of this rank is written, nothing else is.
+    sel = torch.as_tensor(rows - w.P, device=DEV)
+    written = torch.zeros(w.R, dtype=torch.bool, device=DEV)
+    written[sel] = True
+    assert not torch.isnan(out[sel]).any() and not torch.isnan(out_lse[sel]).any()
+    assert torch.isnan(out_lse[~written]).all(), "merge wrote rows of another rank"
+    # Merged pass-KV partials == the all-gathered partial, on every row.
+    o_ag, l_ag = _run_allgather(w, plan, q, k, v, pre)
+    assert float((o_ag - out[sel]).abs().max()) <= O_TOL
+    assert float((l_ag - out_lse[sel]).abs().max()) <= LSE_TOL
+    # Sampled rows against the fp64 oracle.
+    pick = _sample_rows(plan, n_random, w.seed)
+    pos = rows[pick]
+    kk, vv = f64(k), f64(v)
+    kc = vc = bt = None
+    if pre is not None:
+        kc, vc = f64(pre.k_cache), f64(pre.v_cache)
+        bt = pre.block_table.cpu().numpy().astype(np.int64)
+    qq = f64(q[torch.as_tensor(pick, device=DEV)])
+    O_ref, L_ref = oatt.rank_partial(qq, pos, w.P, kk, vv, kc, vc, bt)
+    got = out[torch.as_tensor(pos - w.P, device=DEV)]
+    got_l = out_lse[torch.as_tensor(pos - w.P, device=DEV)]
+    return compare(f64(got), f64(got_l), O_ref, L_ref, f"{name} rank {rank}")
+
+
+def test_llama3_8b_32k_rank0_full_size():
+    _check_workload("llama3_8b_32k_c4", 0, n_random=24)
+
+
+def test_llama3_8b_32k_rank3_full_size():
+    _check_workload("llama3_8b_32k_c4", 3, n_random=8)
+
+
+def test_prefix_hit_64k_full_size():
+    _check_workload("prefix_hit_64k_c2", 0, n_random=8)
+    _check_workload("prefix_hit_64k_c2", 1, n_random=4)
+
+
+def test_llama3_70b_128k_rank0_full_size():
+    _check_workload("llama3_70b_128k_c8", 0, n_random=2)
+
+
+def test_heterogeneous_batch_one_launch():
+    """64 requests, lognormal lengths, per-request C, 19 with a cached prefix
+    in one shared paged pool: every (request, rank) shard in one launch."""
+    Hq, Hkv, D = 32, 8, 128
+    reqs = synth.hetero_requests()
+    total_blocks = sum(P // synth.BLOCK_TOKENS for _, P, _ in reqs) + 32
+    g = synth.generator(2005, device="cuda")
+    k_pool = synth.randn_bf16(g, (total_blocks, synth.BLOCK_TOKENS, Hkv, D), device="cuda")
+    v_pool = synth.randn_bf16(g, (total_blocks, synth.BLOCK_TOKENS, Hkv, D), device="cuda")
+    free = torch.randperm(total_blocks, generator=g, device="cuda")
+    used = 0
+    keep, descs, checks = [], [], []
+    for ri, (L, P, C) in enumerate(reqs):
+        R = L - P
+        q_full, k, v = synth.qkv(g, R, R, Hq, Hkv, D, device="cuda")
+        pre = None
+        if P:
+            pre = synth.paged_prefix(g, P, Hkv, D, device="cuda",
+                                     pool=(k_pool, v_pool, free[used:used + P // synth.BLOCK_TOKENS]))
+            used += P // synth.BLOCK_TOKENS
+        for r in range(C):
+            plan, rows = cp.shard_plan(P, R, C, r)
+            if plan.n_rows == 0:
+                continue
+            q = q_full[torch.as_tensor(rows - P, device=DEV)].contiguous()
+            o = torch.empty((plan.n_rows, Hq, D), dtype=torch.float32, device=DEV)
+            l = torch.empty((plan.n_rows, Hq), dtype=torch.float32, device=DEV)
+            descs.append(cp.make_desc(plan, q, k, v, o, l, k_pool, v_pool,
+                                      pre.block_table if pre else None, include_prefix=True))
+            keep.append((q, o, l))
+            checks.append((ri, P, R, r, plan, rows, q, k, v, pre, o, l))
+    assert sum(L for L, _, _ in reqs) > 100_000
+    ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=DEV)
+    cp.attn_partial(descs, Hq, Hkv, ws)
+    torch.cuda.synchronize()
+    kp, vp = f64(k_pool), f64(v_pool)
+    rng = np.random.default_rng(7)
+    errs = []
+    for ri, P, R, r, plan, rows, q, k, v, pre, o, l in checks:
+        assert not torch.isnan(o).any() and not torch.isnan(l).any()
+        n = plan.n_rows
+        pick = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, size=1)]))
+        pos = rows[pick]
+        bt = pre.block_table.cpu().numpy().astype(np.int64) if pre else None
+        O_ref, L_ref = oatt.rank_partial(f64(q[torch.as_tensor(pick, device=DEV)]), pos, P, f64(k), f64(v),
+                                         kp if pre else None, vp if pre else None, bt)
+        errs.append(compare(f64(o[torch.as_tensor(pick, device=DEV)]), f64(l[torch.as_tensor(pick, device=DEV)]),
+                            O_ref, L_ref, f"request {ri} rank {r}"))
+    assert len(errs) == len(checks)
