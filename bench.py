@@ -49,9 +49,31 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
-                    help="before timing, run one plain device copy of this many MiB, so that a "
-                         "counter profile of the run can scale FETCH_SIZE/WRITE_SIZE by a known size")
+                    help="before timing, copy this many MiB once with lse_merge_kernel over a single "
+                         "partial (plain float4 loads and stores), so that a counter profile of the run "
+                         "can scale FETCH_SIZE/WRITE_SIZE by a known size")
     return ap.parse_args()
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the committed counter profile of
+    this workload, if the kernel source is still the one that was profiled."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    src = os.path.join(ROOT, "paper_2609_04774_amd", "csrc", "attn_partial.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        line = line.strip()
+        if line and not line.startswith("#") and "=" in line:
+            key, val = line.split("=", 1)
+            kv[key] = val
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha:
+        return None
+    return int(kv["fetch_bytes"]) + int(kv["write_bytes"])
 
 
 def main():
@@ -114,12 +136,15 @@ def main():
 
     ws = torch.empty(max(256, cp.workspace_size(make_descs(plan), Hq, Hkv)), dtype=torch.uint8, device=dev)
     if args.copy_calibration_mib > 0:
-        n = args.copy_calibration_mib << 20
-        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        # n_tok rows of 128 fp32 + one fp32 LSE each: (512 + 4) * n_tok bytes in, the same out.
+        n_tok = (args.copy_calibration_mib << 20) // (4 * D)
+        src = torch.ones((n_tok, 1, D), dtype=torch.float32, device=dev)
+        src_l = torch.zeros((n_tok, 1), dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        dst_l = torch.empty_like(src_l)
+        cp.attn_merge([src], [src_l], dst, dst_l)
         torch.cuda.synchronize()
-        del src, dst
+        del src, src_l, dst, dst_l
     stream = torch.cuda.current_stream()
     flop = 4.0 * D * Hq * plan.visible_pairs
 
@@ -195,7 +220,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(w.name) if args.mode == "passkv" and rank == 0 else None,
             "launch_ms": round(attn_ms, 4),
         },
         "merge": {
