@@ -176,7 +176,8 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
  * Each call stages the descriptor copy through pinned host memory owned by
  * the library (allocated on first use, kept until process exit).
  * Errors: CP_ERR_INVALID (shapes, plans, pointers, alignment, kv_rank),
- * CP_ERR_UNSUPPORTED (head_dim), CP_ERR_CAPACITY (workspace), CP_ERR_HIP.
+ * CP_ERR_UNSUPPORTED (head_dim; a request with P + R > 2^30 tokens),
+ * CP_ERR_CAPACITY (workspace), CP_ERR_HIP.
  */
 int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
                     int32_t n_heads_kv, int32_t head_dim, float softmax_scale,

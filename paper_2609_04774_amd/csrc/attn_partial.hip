@@ -7,11 +7,11 @@
 //
 // How (FlashAttention-2 style online softmax, Dao 2023, with the running
 // max/sum recurrence of Milakov & Gimelshein 2018):
-//   * A workgroup (4 wave64s) owns 256 (query, head) rows that share one KV
-//     head: `heads_per_wg` query heads x `q_per_wg` consecutive positions, so
-//     every K/V tile staged in LDS is reused by all of them.  Each wave owns
-//     two blocks of 32 rows.
-//   * Keys are visited in tiles of 64 along each key range (paged prefix,
+//   * A workgroup of 4 wave64s (one per SIMD) owns 256 (query, head) rows that
+//     share one KV head: `heads_per_wg` query heads x `q_per_wg` consecutive
+//     positions.  Each wave owns two blocks of 32 rows, so every K or V
+//     fragment read from LDS feeds two MFMAs.
+//   * Keys are visited in tiles of 32 along each key range (paged prefix,
 //     then the suffix ranges).  Tiles past the workgroup's last query are
 //     never visited; only tiles that cross the diagonal or a range end are
 //     masked.
@@ -20,9 +20,16 @@
 //     row max and row sum are in-lane plus one exchange with lane ^ 32, and
 //     the probabilities feed O^T += V^T P^T directly from registers.  V^T
 //     fragments come from the row-major V tile through ds_read_b64_tr_b16.
+//   * Software pipeline: iteration j runs S_{j+1} = K_{j+1} Q^T, the softmax
+//     of S_j and O += V_{j-1}^T P_{j-1} -- three independent streams -- as
+//     one fixed sequence of MFMA slots with the softmax dealt out between
+//     them, so the matrix cores and the VALU work side by side within each
+//     wave.  Iterations go in pairs that share one workgroup barrier and swap
+//     the two score register sets; each iteration loads tile j+5 into LDS
+//     with loads spread over its slots.
 //   * LDS rows are 256 bytes; 16-byte chunks are XOR-swizzled by the row so
-//     that both the K reads (8 rows, one chunk) and the transposed V reads
-//     (4 rows, two chunks) hit distinct banks.
+//     that both the K reads (16 rows, one chunk) and the transposed V reads
+//     (4 rows, four chunks) hit distinct banks.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -40,7 +47,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kTileKeys = 64;
+constexpr int kWaves = 4;                    // wave64s per workgroup, one per SIMD
+constexpr int kNB = 2;                       // blocks of 32 rows per wave
+constexpr int kTileKeys = 32;
+constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
+constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
 constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 constexpr int kRowBytes = kHeadDim * 2;
 constexpr int kTileBytes = kTileKeys * kRowBytes;
@@ -58,29 +69,52 @@ __device__ __forceinline__ s16x4 ds_read_tr16(const unsigned char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
 
-// Key ranges of one work item: the paged prefix (if read) and up to two
-// suffix ranges, each clipped to the workgroup's last query position.  At
-// most three; selected by a wave-uniform index.
-struct Ranges {
-  int64_t lo[3], hi[3], vis[3];
-  int paged0;  // range 0 is the paged prefix
-  int n;
+// The key tiles of one work item: three ranges in a fixed order -- A, the
+// paged prefix; B and C, the suffix ranges -- each walked in 32-key tiles from
+// `lo` up to `vis` (one past the last key a query of the work item can see);
+// `hi` is the range's end, used for masking.  An unused range has no tiles.
+// Positions are below 2^30 (the host checks), so all of this is 32-bit
+// scalar arithmetic, and a tile is found from its index with selects only.
+// (Plain fields, no arrays: a select between array elements would become an
+// indexed load from scratch memory.)
+struct TileWalk {
+  int hiA;                 // range A is [0, hiA), all visible
+  int loB, hiB, visB;
+  int loC, hiC, visC;
+  int firstB, firstC;      // index of the first tile of ranges B and C
+  int n;                   // tiles over all ranges
 };
 
-struct Cursor {
-  int r;       // range index
-  int64_t t0;  // first key position of the tile
+struct Tile {
+  int t0;    // first key position
+  int hi;    // end of the tile's range
+  int vis;   // visible end of the tile's range
+  bool paged;
 };
 
-__device__ __forceinline__ int64_t sel3(const int64_t (&a)[3], int i) { return i == 0 ? a[0] : (i == 1 ? a[1] : a[2]); }
-
-__device__ __forceinline__ void advance(Cursor& c, const Ranges& rg) {
-  c.t0 += kTileKeys;
-  if (c.t0 >= sel3(rg.vis, c.r)) {
-    ++c.r;
-    c.t0 = sel3(rg.lo, c.r);
-  }
+__device__ __forceinline__ Tile tile_at(const TileWalk w, int t) {
+  const bool gB = t >= w.firstB, gC = t >= w.firstC;
+  Tile x;
+  const int lo = gC ? w.loC : (gB ? w.loB : 0);
+  const int f = gC ? w.firstC : (gB ? w.firstB : 0);
+  x.t0 = lo + (t - f) * kTileKeys;
+  x.hi = gC ? w.hiC : (gB ? w.hiB : w.hiA);
+  x.vis = gC ? w.visC : (gB ? w.visB : w.hiA);
+  x.paged = !gB;
+  return x;
 }
+
+// Descriptor fields the loop needs, read once into registers: the tile loads
+// are inline assembly with a memory clobber, after which the compiler would
+// otherwise load them again from the descriptor on every tile.
+struct KvSource {
+  const unsigned char* k_new;
+  const unsigned char* v_new;
+  const unsigned char* k_cache;
+  const unsigned char* v_cache;
+  const int32_t* block_table;
+  int P;
+};
 
 // One global_load_lds_dwordx4: lane l's 16 bytes at sbase + voff land at LDS
 // byte m0 + 16*l.  Issued as inline assembly so the compiler does not treat
@@ -100,56 +134,73 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
   return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) unsigned char*)p);
 }
 
-// Issues this wave's share of one K/V tile straight into LDS.  Wave w fills
-// tile rows RPW*w .. RPW*w + RPW-1; lane l of load i carries row
-// RPW*w + 4i + l/16, physical chunk l%16, i.e. logical chunk (l%16) ^ swz(row).
-// The address is a wave-uniform base (tile start, KV head) plus a per-lane
-// offset `lane_off[i]` = row_in_tile * row_stride + 16 * logical chunk.  Rows
-// past the visible end read a clamped, in-range row; those keys are masked
-// in the scores.
-template <int RPW>
-__device__ __forceinline__ void issue_tile(const Cursor& c, const Ranges& rg, const DevDesc& d, int kvh,
-                                           int row_stride, int wave, const uint32_t (&lane_off)[RPW / 4],
-                                           const int (&lane_row)[RPW / 4], uint32_t sk, uint32_t sv) {
-  const int64_t vis = sel3(rg.vis, c.r);
-  const bool paged = (c.r == 0) && rg.paged0;
-  const int row0 = wave * RPW;
+// This wave's share of one K/V tile load, prepared ahead of the slots that
+// issue it.  Wave w fills tile rows RPW*w .. RPW*w + RPW-1; lane l of load i
+// carries row RPW*w + 4i + l/16, physical chunk l%16, i.e. logical chunk
+// (l%16) ^ swz(row).  The address is a wave-uniform base (tile start, KV
+// head) plus a per-lane offset `lane_off[i]` = row_in_tile * row_stride + 16 *
+// logical chunk.  In the last tile of a suffix range, rows past the visible
+// end read the last visible row instead (in range; those keys are masked).
+struct TileLoad {
   const unsigned char* kb;
   const unsigned char* vb;
-  int clamp_row = 1 << 30;  // last readable row of this tile, relative to its first row
-  if (paged) {
-    // Prefix tiles start at multiples of 64 keys, so this wave's rows lie in
+  uint32_t off[2];
+  uint32_t lk[2], lv[2];  // LDS destinations of the two row groups
+};
+
+template <int RPW>
+__device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src, int kvh, int row_stride, int wave,
+                                              const uint32_t (&lane_off)[RPW / 4], const int (&lane_row)[RPW / 4],
+                                              const uint32_t (&lane_chunk)[RPW / 4], uint32_t sk, uint32_t sv) {
+  static_assert(RPW == 8, "two row groups of four per wave");
+  const int row0 = wave * RPW;
+  TileLoad t;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    t.off[i] = lane_off[i];
+    t.lk[i] = sk + (uint32_t)((row0 + 4 * i) * kRowBytes);
+    t.lv[i] = sv + (uint32_t)((row0 + 4 * i) * kRowBytes);
+  }
+  if (x.paged) {
+    // Prefix tiles start at multiples of 32 keys, so this wave's rows lie in
     // logical cache block t0/16 + row0/16 (clamped to the last block); the
     // lane offsets use the row within the tile, so step back by the block's
-    // first tile row.
-    int64_t lb = (c.t0 >> 4) + (row0 >> 4);
-    const int64_t last = ((vis + kBlockTokens - 1) >> 4) - 1;
+    // first tile row.  Wave-uniform index: a scalar load.
+    int lb = (x.t0 >> 4) + (row0 >> 4);
+    const int last = ((x.vis + kBlockTokens - 1) >> 4) - 1;
     lb = lb < last ? lb : last;
-    const int64_t blk =
-        __builtin_amdgcn_readfirstlane(((const __attribute__((address_space(1))) int32_t*)d.block_table)[lb]);
+    const int64_t blk = ((const __attribute__((address_space(4))) int32_t*)src.block_table)[lb];
     const int64_t base = (blk * kBlockTokens - (row0 & ~(kBlockTokens - 1))) * row_stride + kvh * (kHeadDim * 2);
-    kb = reinterpret_cast<const unsigned char*>(d.k_cache) + base;
-    vb = reinterpret_cast<const unsigned char*>(d.v_cache) + base;
+    t.kb = src.k_cache + base;
+    t.vb = src.v_cache + base;
   } else {
-    const int64_t base = (c.t0 - d.P) * row_stride + kvh * (kHeadDim * 2);
-    kb = reinterpret_cast<const unsigned char*>(d.k_new) + base;
-    vb = reinterpret_cast<const unsigned char*>(d.v_new) + base;
-    if (c.t0 + kTileKeys > vis) clamp_row = (int)(vis - 1 - c.t0);
-  }
+    const int64_t base = (int64_t)(x.t0 - src.P) * row_stride + kvh * (kHeadDim * 2);
+    t.kb = src.k_new + base;
+    t.vb = src.v_new + base;
+    if (x.t0 + kTileKeys > x.vis) {
+      const int clamp_row = x.vis - 1 - x.t0;
 #pragma unroll
-  for (int i = 0; i < RPW / 4; ++i) {
-    uint32_t off = lane_off[i];
-    if (lane_row[i] > clamp_row) off = off - (uint32_t)((lane_row[i] - clamp_row) * row_stride);
-    const uint32_t lrow = (uint32_t)((row0 + 4 * i) * kRowBytes);
-    dma16(kb, off, sk + lrow);
-    dma16(vb, off, sv + lrow);
+      for (int i = 0; i < 2; ++i) {
+        const int r = lane_row[i] < clamp_row ? lane_row[i] : clamp_row;
+        t.off[i] = __umul24((uint32_t)r, (uint32_t)row_stride) + lane_chunk[i];
+      }
+    }
   }
+  return t;
 }
 
-// Clamps a wave-uniform offset to a range where 32-bit arithmetic with a
-// lane's query index (< 2^16) cannot overflow; results are clamped to a tile.
-__device__ __forceinline__ int clamp_i32(int64_t x) {
-  return (int)(x < -(1 << 24) ? -(1 << 24) : (x > (1 << 24) ? (1 << 24) : x));
+// Load q (0..3) of a prepared tile: K or V rows of group q/2.
+__device__ __forceinline__ void issue_load(const TileLoad& t, int q) {
+  const int i = q >> 1;
+  if (q & 1)
+    dma16(t.vb, t.off[i], t.lv[i]);
+  else
+    dma16(t.kb, t.off[i], t.lk[i]);
+}
+
+__device__ __forceinline__ void issue_tile(const TileLoad& t) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) issue_load(t, q);
 }
 
 __device__ __forceinline__ float xmax32(float x) {
@@ -170,22 +221,18 @@ __device__ __forceinline__ float xsum32(float x) {
 // stay below 256, which bf16 and the fp32 sums hold exactly as well.
 constexpr float kLazyRescaleLog2 = 8.f;
 
-// s_waitcnt immediate for vmcnt(0) with expcnt/lgkmcnt left at their maxima
-// (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt_hi[15:14]).
-constexpr int kWaitVmcnt0 = 0x0F70;
-
 // Per-lane LDS byte offsets of the fragments, relative to a K or V tile.
-//   K (A operand of S^T = K Q^T): lane reads tile row 32kb + l32, logical
-//   chunk 2ds + half.  swz(row) only depends on l32, so key block kb is a
-//   constant +8192 and only the 8 steps ds need their own offset.
+//   K (A operand of S^T = K Q^T): lane reads tile row l32, logical chunk
+//   2ds+half; only the 8 steps ds need their own offset, computed as
+//   krow + ((2ds) ^ kx) * 16.
 //   V (A operand of O^T += V^T P^T, transposed 64-bit reads): for k-step ks
 //   and head-dim block db the group's 16 lanes read rows
 //   kbase + i/4 (kbase = 16ks + 4half, +8 for the second half of the slots) at
 //   columns d0 + 4(i%4), d0 = 32db + 16(group&1).  swz of those rows does not
 //   depend on ks, so ks is a constant +4096 and 4 db x 2 halves need offsets.
 struct FragOffsets {
-  uint32_t krow;  // tile row l32 (key block 0): l32 * 256
-  uint32_t kx;    // swz(l32), the XOR applied to K chunk indices
+  uint32_t krow;
+  uint32_t kx;
   uint32_t v[4][2];
 };
 
@@ -207,60 +254,164 @@ __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
   return f;
 }
 
-// S^T = K Q^T for one 64-key tile: s[kb][b] holds keys 32kb..32kb+31 (rows)
-// against the 32 queries of block b (columns).  K fragments come from the
-// LDS tile (row l32 of key block kb, chunk 2ds+half); the query fragments
-// qf[b][ds] stay in registers for the whole work item.
-template <int NB>
-__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[NB][8],
-                                        f32x16 (&s)[2][NB]) {
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int b = 0; b < NB; ++b) s[kb][b] = f32x16{};
+// One step of S^T = K Q^T written straight to VGPRs (the softmax reads the
+// scores with VALU instructions; the MFMA's own accumulator form would put
+// them in AGPRs and cost a copy per score).  The query fragment stays in
+// AGPRs.  The compiler does not see into the assembly, so readers of `acc`
+// are kept at least 19 wait states away by construction (every caller issues
+// 16 more MFMAs, or an explicit s_nop block, before the scores are read).
+__device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& k, const bf16x8& q, bool first) {
+  if (first)
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "a"(q));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "a"(q));
+}
+
+// Wait states between the last score MFMA of the prologue and the first
+// VALU read of its result (a 32x32x16 MFMA needs at most 19).
+__device__ __forceinline__ void mfma_result_wait() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4"); }
+
+// S^T = K Q^T for one 32-key tile (the prologue's first tile).
+__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
+                                        f32x16 (&s)[kNB]) {
 #pragma unroll
   for (int ds = 0; ds < 8; ++ds) {
-    const uint32_t off = fo.krow + (((uint32_t)(2 * ds) ^ fo.kx) << 4);
+    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + fo.krow + (((uint32_t)(2 * ds) ^ fo.kx) << 4));
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + off + kb * 32 * kRowBytes);
+    for (int b = 0; b < kNB; ++b) mfma_qk(s[b], kf, qf[b][ds], ds == 0);
+  }
+  mfma_result_wait();
+}
+
+// O^T += V^T P^T for one 32-key tile (the last one); each V fragment serves
+// both query blocks.
+__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
+                                        f32x16 (&o)[4][kNB]) {
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        s[kb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[b][ds], s[kb][b], 0, 0, 0);
+  for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
+      const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+      for (int b = 0; b < kNB; ++b) o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
     }
   }
 }
 
-// Masks keys at tile offsets >= lim[b]; accumulator register r of key block
-// kb is tile key 32kb + (r/4)*8 + 4*half + r%4.
-template <int NB>
-__device__ __forceinline__ void mask_tile(f32x16 (&s)[2][NB], int half, const int (&lim)[NB]) {
+// Masks keys at tile offsets >= lim[b]; score register r is tile key
+// (r/4)*8 + 4*half + r%4.
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[kNB], int half, const int (&lim)[kNB]) {
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int r = 0; r < 16; ++r) {
+    const int off = (r >> 2) * 8 + half * 4 + (r & 3);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int off = kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-        if (off >= lim[b]) s[kb][b][r] = -INFINITY;
-    }
+    for (int b = 0; b < kNB; ++b)
+      if (off >= lim[b]) s[b][r] = -INFINITY;
+  }
 }
 
-// Online softmax, first half: the running max of each query column (the two
-// lane halves hold disjoint keys of the same query and always agree on it)
-// and the factor alpha that moves O and the row sums from the old max to
-// the new one.  Returns -max * scale * log2(e), the exponent offset.
-template <int NB>
-__device__ __forceinline__ void softmax_max(const f32x16 (&s)[2][NB], float (&m_run)[NB], float (&l_run)[NB],
-                                            float (&lb_run)[NB], float (&alpha)[NB], float (&neg)[NB], float sl2) {
+// Keys at tile offsets >= lim are past the range end (hi) or after the
+// lane's query (position q0 + qrel).  A tile past the wave's last query is
+// masked entirely.  Returns whether the tile needs masking at all.
+__device__ __forceinline__ bool tile_limits(const Tile& x, int q0, bool wave_active, int wave_lo, int wave_hi,
+                                            const int (&qrel)[kNB], const bool (&valid)[kNB], int (&lim)[kNB]) {
+  const bool live = wave_active && x.t0 <= wave_hi;
+  const int a = q0 + 1 - x.t0;
+  const int h = x.hi - x.t0;
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    float mx = s[0][b][0];
+  for (int b = 0; b < kNB; ++b) {
+    int e = qrel[b] + a < h ? qrel[b] + a : h;
+    e = e < 0 ? 0 : (e > kTileKeys ? kTileKeys : e);
+    lim[b] = (live && valid[b]) ? e : 0;
+  }
+  return !live || (x.t0 + kTileKeys > x.hi) || (x.t0 + kTileKeys - 1 > wave_lo);
+}
+
+// O *= alpha (per query column), in place in the accumulation registers, for
+// the rare softmax that moved the running max.  Each element goes through a
+// VGPR inside one asm statement so that O keeps living in AGPRs (a VALU
+// multiply in plain code would make the compiler move all of O to VGPRs and
+// back on every iteration).  The s_nop blocks keep the matrix-core hazards:
+// the last MFMA's results land before they are read, and the writes before
+// the next MFMA reads them.
+__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alpha)[kNB]) {
+  bool any = false;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+  for (int b = 0; b < kNB; ++b) any |= alpha[b] != 1.f;
+  if (__any(any)) {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4");
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = __builtin_fmaxf(mx, s[kb][b][r]);
-    mx = xmax32(mx);
+    for (int b = 0; b < kNB; ++b)
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float x = o[db][b][r];
+          float t;
+          asm volatile(
+              "v_accvgpr_read_b32 %1, %0\n\t"
+              "v_mul_f32 %1, %1, %2\n\t"
+              "v_accvgpr_write_b32 %0, %1"
+              : "+a"(x), "=&v"(t)
+              : "v"(alpha[b]));
+          o[db][b][r] = x;
+        }
+    asm volatile("s_nop 7");
+  }
+}
+
+// One iteration's matrix and vector work as a fixed sequence of 32 MFMA
+// slots: slots 0-15 compute S_{j+1} = K_{j+1} Q^T (K step d = slot/2 feeds
+// both query blocks), slots 16-31 add P_{j-1} V_{j-1} (V fragment slot/2 - 8).
+// The softmax of S_j is cut into units of roughly equal VALU time and dealt
+// out over the slots, so that every MFMA has vector work to overlap with;
+// LDS fragments are read three fragments (six slots) ahead, and the four
+// loads of tile j+5 go out at slots 1, 9, 17 and 25.  Scheduling barriers
+// keep the slots in this order.
+//
+// Units: 0-7 running max over four scores (block u/4), 8-9 the exchange with
+// the other lane half and the new max / rescale factor of block u-8, then per
+// block 8 x (two exponentials, one pack-and-sum) for score pairs.
+constexpr int kUnits = 58;
+constexpr int kSlotFirstUnit[33] = {0,  4,  8,  9,  10, 12, 13, 15, 17, 19, 20, 22, 24, 25, 27, 29, 31,
+                                    32, 34, 36, 37, 39, 41, 43, 44, 46, 48, 49, 51, 53, 55, 56, 58};
+constexpr int kLookahead = 3;
+
+// Forces `x` to be computed before this point: an empty volatile asm that
+// reads it stays in program order with the scheduling barriers, so the
+// value's producers cannot sink past the slot they were written in.
+template <typename T>
+__device__ __forceinline__ void pin(const T& x) {
+  asm volatile("" ::"v"(x));
+}
+
+struct SoftmaxState {
+  float mx[kNB];   // partial max of the tile's scores
+  float neg[kNB];  // -m * scale * log2(e)
+  float rs[kNB];   // fp32 sum of this tile's probabilities
+  float rsb[kNB];  // sum of the bf16-rounded probabilities
+  bf16x2 pp[kNB][8];
+};
+
+__device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxState& st, float (&m_run)[kNB],
+                                             float (&l_run)[kNB], float (&lb_run)[kNB], float (&alpha)[kNB],
+                                             float sl2) {
+  if (u < 8) {
+    const int b = u >> 2, q = (u & 3) * 4;
+    if (q == 0) {
+      st.mx[b] = __builtin_fmaxf(__builtin_fmaxf(s[b][0], s[b][1]), __builtin_fmaxf(s[b][2], s[b][3]));
+    } else {
+      st.mx[b] = __builtin_fmaxf(__builtin_fmaxf(st.mx[b], s[b][q]),
+                                 __builtin_fmaxf(s[b][q + 1], __builtin_fmaxf(s[b][q + 2], s[b][q + 3])));
+    }
+    pin(st.mx[b]);
+  } else if (u < 10) {
+    // Both lane halves hold disjoint keys of the same query and agree on the
+    // max after the exchange.
+    const int b = u - 8;
+    const float mx = xmax32(st.mx[b]);
     const float m_new = __builtin_fmaxf(m_run[b], mx);
     const bool grow = (m_new - m_run[b]) * sl2 > kLazyRescaleLog2;
     const float m_upd = grow ? m_new : m_run[b];
@@ -268,156 +419,95 @@ __device__ __forceinline__ void softmax_max(const f32x16 (&s)[2][NB], float (&m_
     m_run[b] = m_upd;
     l_run[b] *= alpha[b];
     lb_run[b] *= alpha[b];
-    neg[b] = (m_upd == -INFINITY) ? 0.f : -m_upd * sl2;
-  }
-}
-
-// Online softmax, second half: the probabilities of the tile, rounded to
-// bf16 once for the PV product, as P^T fragments.  Two row sums: the fp32 one
-// gives the LSE, the sum of the rounded values (v_dot2 against (1, 1))
-// normalises O, so that O's numerator and denominator use the same weights
-// (exact for a single dominant key).  Fragment ks covers tile keys
-// 16ks..16ks+15; its slot t of lane half h is key 16ks + (t/4)*8 + 4h + t%4,
-// i.e. accumulator register 8*(ks%2) + t of key block ks/2.
-template <int NB>
-__device__ __forceinline__ void softmax_probs(const f32x16 (&s)[2][NB], const float (&neg)[NB], float (&l_run)[NB],
-                                              float (&lb_run)[NB], bf16x8 (&pf)[NB][4], float sl2) {
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    float rs = 0.f;
-    float rsb = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      bf16x2 pp[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks >> 1][b][8 * (ks & 1) + 2 * t], sl2, neg[b]));
-        const float e1 =
-            __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks >> 1][b][8 * (ks & 1) + 2 * t + 1], sl2, neg[b]));
-        pp[t] = bf16x2{(__bf16)e0, (__bf16)e1};
-        rs += e0 + e1;
-        rsb = __builtin_amdgcn_fdot2_f32_bf16(pp[t], kOnes, rsb, false);
-      }
-      pf[b][ks] = __builtin_shufflevector(__builtin_shufflevector(pp[0], pp[1], 0, 1, 2, 3),
-                                          __builtin_shufflevector(pp[2], pp[3], 0, 1, 2, 3), 0, 1, 2, 3, 4, 5, 6,
-                                          7);
-    }
-    l_run[b] += rs;
-    lb_run[b] += rsb;
-  }
-}
-
-// O^T += V^T P^T for one tile.  The transposed V read gives lane (group g,
-// index i) the four keys kbase..kbase+3 of column d0 + i (see FragOffsets).
-template <int NB>
-__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[NB][4],
-                                        f32x16 (&o)[4][NB]) {
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-    for (int db = 0; db < 4; ++db) {
-      const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
-      const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
-      const s16x8 v8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, v8);
-#pragma unroll
-      for (int b = 0; b < NB; ++b) o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
+    st.neg[b] = (m_upd == -INFINITY) ? 0.f : -m_upd * sl2;
+    st.rs[b] = 0.f;
+    st.rsb[b] = 0.f;
+    pin(st.neg[b]);
+  } else {
+    const int e = u - 10, b = e / 24, r = e % 24, t = r / 3, kind = r % 3;
+    if (kind < 2) {
+      const int i = 2 * t + kind;
+      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], sl2, st.neg[b]));
+      pin(x);
+      s[b][i] = x;
+    } else {
+      const bf16x2 pp = bf16x2{(__bf16)s[b][2 * t], (__bf16)s[b][2 * t + 1]};
+      st.pp[b][t] = pp;
+      st.rs[b] += s[b][2 * t] + s[b][2 * t + 1];
+      st.rsb[b] = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb[b], false);
+      pin(st.rs[b]);
+      pin(st.rsb[b]);
+      pin(pp);
     }
   }
 }
 
-// MFMA phase M_j of one wave: O += V_{j-1}^T P_{j-1}, then S_j = K_j Q^T,
-// then the mask of
-// S_j: keys at tile offsets >= lim are past the key range end (hi) or after
-// the lane's query (position q0 + qrel) and get -inf.
-template <int NB>
-__device__ __forceinline__ void mfma_phase(const unsigned char* sv_prev, const bf16x8 (&pf)[NB][4],
-                                           const unsigned char* sk, const bf16x8 (&qf)[NB][8], const FragOffsets& fo,
-                                           int64_t t0, int64_t hi, int64_t q0, bool wave_active, int64_t wave_lo,
-                                           int64_t wave_hi, const int (&qrel)[NB], const bool (&valid)[NB],
-                                           f32x16 (&o)[4][NB], f32x16 (&s)[2][NB]) {
-  // Straight-line on purpose (one scheduling region): before the first tile
-  // P is zero against tile 0's finite V, and a tile past the wave's last
-  // query is multiplied anyway and then fully masked.
-  const bool live = wave_active && t0 <= wave_hi;
-  pv_tile<NB>(sv_prev, fo, pf, o);
-  qk_tile<NB>(sk, fo, qf, s);
-  // Read-ahead: four V fragments (two transposed reads each) ahead of the
-  // PV MFMAs; the first four d-steps of K (two reads each) under the last four
-  // PV MFMAs; then one K read per QK MFMA, which keeps K eight MFMAs ahead.
-  static_assert(NB == 1, "schedule written for one 32-row block per wave");
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+// Fragment g of the region: g < 8 is K step g, g >= 8 is V^T fragment
+// (k-step (g-8)/4, d-block (g-8)%4).
+__device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, const unsigned char* sk,
+                                            const FragOffsets& fo) {
+  if (g < 8) return *reinterpret_cast<const bf16x8*>(sk + fo.krow + (((uint32_t)(2 * g) ^ fo.kx) << 4));
+  const int ks = (g - 8) >> 2, db = (g - 8) & 3;
+  const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
+  const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// s_in: S_j (masked), turned into P_j; s_out: receives S_{j+1}.  pf: P_{j-1}
+// on entry, P_j on exit.
+__device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
+                                                 const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
+                                                 bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB],
+                                                 f32x16 (&s_out)[kNB], float (&m_run)[kNB], float (&l_run)[kNB],
+                                                 float (&lb_run)[kNB], float (&alpha)[kNB], float sl2,
+                                                 const TileLoad& ld) {
+  SoftmaxState st;
+  bf16x8 fr[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
+  for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  if (!live || (t0 + kTileKeys > hi) || (t0 + kTileKeys - 1 > wave_lo)) {
-    // lim = min(pos + 1, hi) - t0 in 32 bits from two clamped uniform offsets.
-    const int a32 = clamp_i32(q0 + 1 - t0);
-    const int b32 = clamp_i32(hi - t0);
-    int lim[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      int e = qrel[b] + a32 < b32 ? qrel[b] + a32 : b32;
-      e = e < 0 ? 0 : (e > kTileKeys ? kTileKeys : e);
-      lim[b] = (live && valid[b]) ? e : 0;
+  for (int slot = 0; slot < 32; ++slot) {
+    if ((slot & 1) == 0 && slot / 2 + kLookahead < 16)
+      fr[slot / 2 + kLookahead] = load_frag(slot / 2 + kLookahead, sv, sk, fo);
+    if ((slot & 7) == 1) issue_load(ld, slot >> 3);
+    const int b = slot & 1;
+    if (slot < 16) {
+      const int d = slot >> 1;
+      mfma_qk(s_out[b], fr[d], qf[b][d], d == 0);
+    } else {
+      const int f = (slot >> 1) - 8;
+      o[f & 3][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[8 + f], pf[b][f >> 2], o[f & 3][b], 0, 0, 0);
     }
-    mask_tile<NB>(s, (threadIdx.x & 32) ? 1 : 0, lim);
+#pragma unroll
+    for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
+      softmax_unit(u, s_in, st, m_run, l_run, lb_run, alpha, sl2);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int b = 0; b < kNB; ++b) {
+    l_run[b] += st.rs[b];
+    lb_run[b] += st.rsb[b];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+      pf[b][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[b][4 * ks], st.pp[b][4 * ks + 1], 0, 1, 2, 3),
+                                          __builtin_shufflevector(st.pp[b][4 * ks + 2], st.pp[b][4 * ks + 3], 0, 1, 2, 3),
+                                          0, 1, 2, 3, 4, 5, 6, 7);
   }
 }
 
-// VALU phase V_j: softmax of S_j, rescale of O to the new running max (O
-// holds every tile up to j-1 at this point), probabilities P_j.
-template <int NB>
-__device__ __forceinline__ void valu_phase(const f32x16 (&s)[2][NB], float (&m_run)[NB], float (&l_run)[NB],
-                                           float (&lb_run)[NB], bf16x8 (&pf)[NB][4], f32x16 (&o)[4][NB], float sl2) {
-  float alpha[NB], neg[NB];
-  softmax_max<NB>(s, m_run, l_run, lb_run, alpha, neg, sl2);
-  bool rescale = false;
-#pragma unroll
-  for (int b = 0; b < NB; ++b) rescale |= alpha[b] != 1.f;
-  if (__any(rescale)) {
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) o[db][b] *= alpha[b];
-  }
-  softmax_probs<NB>(s, neg, l_run, lb_run, pf, sl2);
-}
+// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
+// vmcnt_hi[15:14]) waiting until at most N of this wave's vector-memory
+// operations are outstanding.
+constexpr int kLoadsPerTile = 4;  // K and V loads of one tile per wave
+constexpr int kWaitVm(int n) { return 0x0F70 | n; }
 
-// Barrier j+1 of the tile loop: this wave's loads of tile j+1 are complete
-// (so after the barrier everyone's are), and every wave is past its reads of
-// K_j and V_{j-1}, whose buffers tile j+2 then reuses.
-template <int RPW>
-__device__ __forceinline__ void barrier_and_prefetch(int j, int n_tiles, Cursor& lc, const Ranges& rg,
-                                                     const DevDesc& d, int kvh, int row_stride, int wave,
-                                                     const uint32_t (&lane_off)[RPW / 4],
-                                                     const int (&lane_row)[RPW / 4], uint32_t lk0, uint32_t lv0) {
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  __syncthreads();
-  if (j + 2 < n_tiles) {
-    advance(lc, rg);
-    issue_tile<RPW>(lc, rg, d, kvh, row_stride, wave, lane_off, lane_row, lk0 + ((j + 2) % 2) * kTileBytes,
-                    lv0 + ((j + 2) % 3) * kTileBytes);
-  }
-}
-
-// NB = blocks of 32 rows per wave; 8/NB waves cover the workgroup's 256 rows.
-template <int NB>
-__global__ __launch_bounds__(64 * (8 / NB), 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
-                                                                        const WorkItem* __restrict__ items,
-                                                                        PartialParams p) {
-  constexpr int kWaves = 8 / NB;
+__global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
+                                                                     const WorkItem* __restrict__ items,
+                                                                     PartialParams p) {
   constexpr int kRPW = kTileKeys / kWaves;  // tile rows each wave loads
-  // LDS: two K tile buffers, then three V tile buffers.
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[5 * kTileBytes];
+  // LDS: kBufs K tile buffers, then kBufs V tile buffers; tile t uses buffer
+  // t % kBufs of each.
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kBufs * kTileBytes];
 
   const WorkItem it = items[blockIdx.x];
   const DevDesc& d = descs[it.desc];
@@ -427,30 +517,31 @@ __global__ __launch_bounds__(64 * (8 / NB), 1) void attn_partial_kernel(const De
   const int half = lane >> 5;
   const int l32 = lane & 31;
 
-  const int64_t q_begin = it.chunk ? d.q_begin[1] : d.q_begin[0];
-  const int64_t q_len = it.chunk ? d.q_len[1] : d.q_len[0];
+  // Positions are below 2^30 (checked on the host): 32 bits suffice.
+  const int q_begin = (int)(it.chunk ? d.q_begin[1] : d.q_begin[0]);
+  const int q_len = (int)(it.chunk ? d.q_len[1] : d.q_len[0]);
   const int64_t loff = it.chunk ? d.local_off[1] : d.local_off[0];
   const int Hq = p.Hq;
   const int Hkv = p.Hkv;
   const int kvh = it.head_group / p.groups_per_kv;
   const int head0 = kvh * (Hq / Hkv) + (it.head_group % p.groups_per_kv) * p.heads_per_wg;
   const int qblocks_per_head = p.q_per_wg >> 5;
-  const int64_t qb0 = (int64_t)it.q_block * p.q_per_wg;
-  const int64_t wg_last = (qb0 + p.q_per_wg < q_len ? qb0 + p.q_per_wg : q_len) - 1;
-  const int64_t wg_pos_hi = q_begin + wg_last;
+  const int qb0 = it.q_block * p.q_per_wg;
+  const int wg_last = (qb0 + p.q_per_wg < q_len ? qb0 + p.q_per_wg : q_len) - 1;
+  const int wg_pos_hi = q_begin + wg_last;
 
-  int head_b[NB];
-  int qrel_b[NB];  // query index relative to the workgroup's first query
-  bool valid_b[NB];
-  int64_t wave_lo = INT64_MAX, wave_hi = -1;
+  int head_b[kNB];
+  int qrel_b[kNB];  // query index relative to the workgroup's first query
+  bool valid_b[kNB];
+  int wave_lo = INT32_MAX, wave_hi = -1;
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int bi = NB * wave + b;
+  for (int b = 0; b < kNB; ++b) {
+    const int bi = kNB * wave + b;
     head_b[b] = head0 + bi / qblocks_per_head;
     const int qo = (bi % qblocks_per_head) * 32;
     qrel_b[b] = qo + l32;
     valid_b[b] = qb0 + qrel_b[b] < q_len;
-    const int64_t blo = qb0 + qo, bhi = (qb0 + qo + 31 < wg_last ? qb0 + qo + 31 : wg_last);
+    const int blo = qb0 + qo, bhi = (qb0 + qo + 31 < wg_last ? qb0 + qo + 31 : wg_last);
     if (blo <= wg_last) {
       wave_lo = (q_begin + blo < wave_lo) ? q_begin + blo : wave_lo;
       wave_hi = (q_begin + bhi > wave_hi) ? q_begin + bhi : wave_hi;
@@ -458,126 +549,147 @@ __global__ __launch_bounds__(64 * (8 / NB), 1) void attn_partial_kernel(const De
   }
   const bool wave_active = wave_hi >= 0;
 
-  // Key ranges and the number of 64-key tiles over all of them.
-  Ranges rg;
-  rg.n = 0;
-  rg.paged0 = 0;
-  int n_tiles = 0;
-#pragma unroll
-  for (int i = 0; i < 3; ++i) rg.lo[i] = rg.hi[i] = rg.vis[i] = 0;
-  if (d.prefix_keys > 0) {
-    rg.lo[0] = 0;
-    rg.hi[0] = rg.vis[0] = d.prefix_keys;
-    rg.paged0 = 1;
-    rg.n = 1;
-    n_tiles += (int)((d.prefix_keys + kTileKeys - 1) / kTileKeys);
+  // Key ranges (prefix, then the suffix ranges clipped to the workgroup's
+  // last query) and their tiles.
+  TileWalk tw;
+  {
+    const int nA = (d.prefix_keys + kTileKeys - 1) / kTileKeys;  // 0 when the prefix is not read
+    tw.hiA = d.prefix_keys;
+    tw.loB = (int)d.seg_lo[0];
+    tw.hiB = (int)d.seg_hi[0];
+    tw.visB = tw.hiB < wg_pos_hi + 1 ? tw.hiB : wg_pos_hi + 1;
+    tw.loC = (int)d.seg_lo[1];
+    tw.hiC = (int)d.seg_hi[1];
+    tw.visC = tw.hiC < wg_pos_hi + 1 ? tw.hiC : wg_pos_hi + 1;
+    const int nB = (d.n_seg > 0 && tw.visB > tw.loB) ? (tw.visB - tw.loB + kTileKeys - 1) / kTileKeys : 0;
+    const int nC = (d.n_seg > 1 && tw.visC > tw.loC) ? (tw.visC - tw.loC + kTileKeys - 1) / kTileKeys : 0;
+    tw.firstB = nA;
+    tw.firstC = nA + nB;
+    tw.n = nA + nB + nC;
   }
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    if (s < d.n_seg) {
-      const int64_t lo = s ? d.seg_lo[1] : d.seg_lo[0];
-      const int64_t hi = s ? d.seg_hi[1] : d.seg_hi[0];
-      const int64_t vis = hi < wg_pos_hi + 1 ? hi : wg_pos_hi + 1;
-      if (vis > lo) {
-        if (rg.n == 0) {
-          rg.lo[0] = lo; rg.hi[0] = hi; rg.vis[0] = vis;
-        } else if (rg.n == 1) {
-          rg.lo[1] = lo; rg.hi[1] = hi; rg.vis[1] = vis;
-        } else {
-          rg.lo[2] = lo; rg.hi[2] = hi; rg.vis[2] = vis;
-        }
-        ++rg.n;
-        n_tiles += (int)((vis - lo + kTileKeys - 1) / kTileKeys);
-      }
-    }
-  }
+  const int n_tiles = tw.n;
 
-  Cursor cc{0, rg.lo[0]};
-  Cursor lc = cc;
-  // Per-lane part of the tile load addresses (see issue_tile).
+  KvSource src;
+  src.k_new = reinterpret_cast<const unsigned char*>(d.k_new);
+  src.v_new = reinterpret_cast<const unsigned char*>(d.v_new);
+  src.k_cache = reinterpret_cast<const unsigned char*>(d.k_cache);
+  src.v_cache = reinterpret_cast<const unsigned char*>(d.v_cache);
+  src.block_table = d.block_table;
+  src.P = (int)d.P;
+
+  // Per-lane part of the tile load addresses (see prep_tile).
   const int row_stride = Hkv * kHeadDim * 2;
-  uint32_t lane_off[kRPW / 4];
+  uint32_t lane_off[kRPW / 4], lane_chunk[kRPW / 4];
   int lane_row[kRPW / 4];
 #pragma unroll
   for (int i = 0; i < kRPW / 4; ++i) {
     const int row = wave * kRPW + 4 * i + (lane >> 4);
     lane_row[i] = row;
-    lane_off[i] = (uint32_t)(row * row_stride + (((lane & 15) ^ swz(row)) << 4));
+    lane_chunk[i] = (uint32_t)(((lane & 15) ^ swz(row)) << 4);
+    lane_off[i] = (uint32_t)(row * row_stride) + lane_chunk[i];
   }
   const uint32_t lds0 = lds_addr(smem);
-  unsigned char* const sk0 = smem;                    // K buffer b at sk0 + b * kTileBytes (b < 2)
-  unsigned char* const sv0 = smem + 2 * kTileBytes;   // V buffer b at sv0 + b * kTileBytes (b < 3)
-  const uint32_t lk0 = lds0, lv0 = lds0 + 2 * kTileBytes;
-  if (n_tiles > 0) issue_tile<kRPW>(lc, rg, d, kvh, row_stride, wave, lane_off, lane_row, lk0, lv0);
+  const unsigned char* const sk0 = smem;
+  const unsigned char* const sv0 = smem + kBufs * kTileBytes;
+  const uint32_t lk0 = lds0, lv0 = lds0 + kBufs * kTileBytes;
+  // Tile t's load (t past the last tile: the last tile again, into a buffer
+  // nobody reads, so that every iteration issues the same loads and the
+  // waits can count them).
+  auto load_of = [&](int t) {
+    const int tt = t < n_tiles ? t : n_tiles - 1;
+    return prep_tile<kRPW>(tile_at(tw, tt), src, kvh, row_stride, wave, lane_off, lane_row, lane_chunk,
+                           lk0 + (t & (kBufs - 1)) * kTileBytes, lv0 + (t & (kBufs - 1)) * kTileBytes);
+  };
+  if (n_tiles > 0) issue_tile(load_of(0));
 
   // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
   // head-dim values of its query, for each of the 8 steps of 16 along D.
   // Rows past the chunk's end are zero and masked out of every tile.
-  bf16x8 qf[NB][8];
+  bf16x8 qf[kNB][8];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
+  for (int b = 0; b < kNB; ++b) {
+    const int64_t qrow_i = loff + (valid_b[b] ? qb0 + qrel_b[b] : qb0);
     const __attribute__((address_space(1))) bf16x8* qrow =
-        (const __attribute__((address_space(1))) bf16x8*)(d.q + ((loff + qb0 + qrel_b[b]) * Hq + head_b[b]) * kHeadDim +
-                                                          half * 8);
+        (const __attribute__((address_space(1))) bf16x8*)(d.q + (qrow_i * Hq + head_b[b]) * kHeadDim + half * 8);
 #pragma unroll
-    for (int ds = 0; ds < 8; ++ds) qf[b][ds] = valid_b[b] ? qrow[2 * ds] : bf16x8{};
+    for (int ds = 0; ds < 8; ++ds) {
+      const bf16x8 v = qrow[2 * ds];
+      qf[b][ds] = valid_b[b] ? v : bf16x8{};
+    }
   }
-
-  // Query rows and tile 0 land before the first barrier of the loop.
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-
-  f32x16 o[4][NB];
-  float m_run[NB], l_run[NB], lb_run[NB];  // running max; sums of fp32 / bf16-rounded probabilities
+  // The query fragments are only ever an MFMA operand: keep them in the
+  // accumulation register file, leaving the VGPRs to the softmax.  (After
+  // all loads are out, so that they overlap.)
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
+  for (int b = 0; b < kNB; ++b)
+#pragma unroll
+    for (int ds = 0; ds < 8; ++ds) asm volatile("" : "+a"(qf[b][ds]));
+  // Query fragments and tile 0 have landed (the builtin form lets the
+  // compiler's own wait tracking see it); then tiles 1..kAhead-1 stream in.
+  __builtin_amdgcn_s_waitcnt(kWaitVm(0));
+  if (n_tiles > 0)
+    for (int t = 1; t < kAhead; ++t) issue_tile(load_of(t));
+
+  const FragOffsets fo = frag_offsets(lane);
+  const float sl2 = p.scale_log2;
+  f32x16 o[4][kNB];
+  float m_run[kNB], l_run[kNB], lb_run[kNB];  // running max; sums of fp32 / bf16-rounded probabilities
+  float alpha[kNB];                            // rescale factor of the last softmax
+  bf16x8 pf[kNB][2];                           // P of the previous tile
+#pragma unroll
+  for (int b = 0; b < kNB; ++b) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
     m_run[b] = -INFINITY;
     l_run[b] = 0.f;
     lb_run[b] = 0.f;
+    alpha[b] = 1.f;
+    pf[b][0] = pf[b][1] = bf16x8{};
   }
-  const float sl2 = p.scale_log2;
+  // Scores of the current tile alternate between two register sets.
+  f32x16 sa[kNB], sb[kNB];
+  const int q0 = q_begin + qb0;
 
-  // Two groups, one instruction stream, shifted barriers.  Every wave runs
-  // M_0 V_0 M_1 V_1 ... M_n with M_j = {O += V_{j-1}^T P_{j-1}, S_j = K_j Q^T}
-  // on the matrix cores and V_j = {softmax of S_j -> P_j} on the VALU.  Waves
-  // 0..3 meet the per-tile barrier after V_j, waves 4..7 after M_j, so between
-  // two barriers group 0 runs M_j then V_j while group 1 runs V_{j-1} then
-  // M_j.  Wave w shares its SIMD with wave w +- 4, so each SIMD pairs one
-  // wave's MFMA phase with the other's softmax.  Tile j+1 is issued right
-  // after barrier j and awaited before barrier j+1; two K buffers and three V
-  // buffers (V_{j-1} is read during interval j).
-  const int group = wave >> 2;
-  const FragOffsets fo = frag_offsets(lane);
-  f32x16 s[2][NB];
-  bf16x8 pf[NB][4];
-#pragma unroll
-  for (int b = 0; b < NB; ++b)
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) pf[b][ks] = bf16x8{};
+  __syncthreads();  // tile 0 is in LDS for everyone
+  if (n_tiles > 0) qk_tile(sk0, fo, qf, sa);
 
-  // Barrier 0: tile 0 and the query rows are in LDS; tile 1 streams in.
-  __syncthreads();
-  if (n_tiles > 1) {
-    advance(lc, rg);
-    issue_tile<kRPW>(lc, rg, d, kvh, row_stride, wave, lane_off, lane_row, lk0 + kTileBytes, lv0 + kTileBytes);
+  // Iteration j: mask S_j, then the region (S_{j+1}, softmax of S_j,
+  // P_{j-1} V_{j-1}, loads of tile j+kAhead), then O's rescale if the max
+  // moved.  Tile 0 has no predecessor: P is zero then, read against V_0's
+  // finite data.
+  auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
+    int lim[kNB];
+    if (tile_limits(tile_at(tw, j), q0, wave_active, wave_lo, wave_hi, qrel_b, valid_b, lim))
+      mask_tile(s_in, half, lim);
+    const TileLoad ld = load_of(j + kAhead);
+    // The last iteration recomputes scores of its own tile (unused).
+    const int kn = j + 1 < n_tiles ? j + 1 : j;
+    const int vp = j > 0 ? j - 1 : 0;
+    pipelined_region(sv0 + (vp & (kBufs - 1)) * kTileBytes, sk0 + (kn & (kBufs - 1)) * kTileBytes, fo, qf, pf, o,
+                     s_in, s_out, m_run, l_run, lb_run, alpha, sl2, ld);
+    rescale_o(o, alpha);
+  };
+
+  // Iterations go in pairs behind one barrier.  At a pair's start every tile
+  // up to j+2 must have landed (both iterations read the K tile after their
+  // own); the two tiles issued after those may still be in flight.  After the
+  // barrier every wave is also done with the iterations before the pair, the
+  // last readers of the buffers its loads reuse (tile j+5 takes tile j-3's).
+  for (int j = 0; j < n_tiles; j += 2) {
+    __builtin_amdgcn_s_waitcnt(kWaitVm(2 * kLoadsPerTile));
+    __syncthreads();
+    iteration(j, sa, sb);
+    if (j + 1 >= n_tiles) break;
+    iteration(j + 1, sb, sa);
   }
-  for (int j = 0; j < n_tiles; ++j) {
-    const int64_t t0 = cc.t0;
-    const int64_t hi = sel3(rg.hi, cc.r);
-    advance(cc, rg);
-    mfma_phase<NB>(sv0 + (j >= 1 ? (j - 1) % 3 : 0) * kTileBytes, pf, sk0 + (j % 2) * kTileBytes, qf, fo, t0, hi,
-                   q_begin + qb0, wave_active, wave_lo, wave_hi, qrel_b, valid_b, o, s);
-    if (group == 1) barrier_and_prefetch<kRPW>(j, n_tiles, lc, rg, d, kvh, row_stride, wave, lane_off, lane_row, lk0, lv0);
-    valu_phase<NB>(s, m_run, l_run, lb_run, pf, o, sl2);
-    if (group == 0) barrier_and_prefetch<kRPW>(j, n_tiles, lc, rg, d, kvh, row_stride, wave, lane_off, lane_row, lk0, lv0);
-  }
-  if (n_tiles > 0) pv_tile<NB>(sv0 + ((n_tiles - 1) % 3) * kTileBytes, fo, pf, o);
+  // No tile load may still be writing LDS when the workgroup ends.
+  __builtin_amdgcn_s_waitcnt(kWaitVm(0));
+  if (n_tiles > 0) pv_tile(sv0 + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
+  for (int b = 0; b < kNB; ++b) {
     const float lt = xsum32(l_run[b]);
     const float ltb = xsum32(lb_run[b]);
     const bool live = (m_run[b] != -INFINITY) && (lt > 0.f) && (ltb > 0.f);
@@ -605,7 +717,7 @@ __global__ __launch_bounds__(64 * (8 / NB), 1) void attn_partial_kernel(const De
 
 int launch_partial(const PartialParams& p, void* stream) {
   if (p.n_items == 0) return CP_OK;
-  hipLaunchKernelGGL(attn_partial_kernel<1>, dim3((unsigned)p.n_items), dim3(512), 0, (hipStream_t)stream,
+  hipLaunchKernelGGL(attn_partial_kernel, dim3((unsigned)p.n_items), dim3(64 * kWaves), 0, (hipStream_t)stream,
                      p.descs, p.items, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial launch: ") + hipGetErrorString(e));

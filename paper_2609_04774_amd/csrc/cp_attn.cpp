@@ -69,6 +69,8 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
   if (!plan_equal(ref, pl)) return fail(CP_ERR_INVALID, who + "plan does not match cp_shard_plan(P, R, C, rank)");
   if (pl.n_rows > ((int64_t)1 << 31)) return fail(CP_ERR_UNSUPPORTED, who + "more than 2^31 rows");
   const int64_t P = pl.prefix_len, R = pl.new_len;
+  // The kernel walks key and query positions in 32-bit arithmetic.
+  if (P + R > ((int64_t)1 << 30)) return fail(CP_ERR_UNSUPPORTED, who + "sequence beyond 2^30 tokens");
   if (x.kv_rank < CP_KV_NONE || x.kv_rank >= pl.C) return fail(CP_ERR_INVALID, who + "kv_rank out of range");
   if (x.include_prefix != 0 && x.include_prefix != 1) return fail(CP_ERR_INVALID, who + "include_prefix must be 0 or 1");
   if (pl.n_rows > 0) {
@@ -304,7 +306,7 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
   p.groups_per_kv = plan.shape.groups_per_kv;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.waves_per_wg = 8;
+  p.waves_per_wg = 4;
   st = launch_partial(p, stream);
   if (st == CP_OK) clear_error();
   return st;

@@ -150,10 +150,12 @@ def _partial_status(descs, Hq=8, Hkv=2, D=128, ws=FAKE * 16, ws_bytes=1 << 30):
     ("workspace too small", {}, {"ws_bytes": 16}, cp.CP_ERR_CAPACITY),
     ("workspace null", {}, {"ws": None}, cp.CP_ERR_INVALID),
     ("workspace misaligned", {}, {"ws": FAKE + 64}, cp.CP_ERR_INVALID),
+    ("sequence beyond 2^30 tokens", {"P": 1 << 30, "R": 64}, {}, cp.CP_ERR_UNSUPPORTED),
 ])
 def test_partial_argument_errors(case, kw, args, status):
     P = kw.pop("P", 0)
-    d = _desc(P=P, **kw)
+    R = kw.pop("R", 64)
+    d = _desc(P=P, R=R, **kw)
     assert _partial_status([d], **args) == status, case
     assert cp.last_error() != ""
 
