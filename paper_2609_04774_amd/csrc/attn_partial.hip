@@ -371,12 +371,16 @@ __device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alp
 // loads of tile j+5 go out at slots 1, 9, 17 and 25.  Scheduling barriers
 // keep the slots in this order.
 //
-// Units: 0-7 running max over four scores (block u/4), 8-9 the exchange with
-// the other lane half and the new max / rescale factor of block u-8, then per
-// block 8 x (two exponentials, one pack-and-sum) for score pairs.
-constexpr int kUnits = 58;
-constexpr int kSlotFirstUnit[33] = {0,  4,  8,  9,  10, 12, 13, 15, 17, 19, 20, 22, 24, 25, 27, 29, 31,
-                                    32, 34, 36, 37, 39, 41, 43, 44, 46, 48, 49, 51, 53, 55, 56, 58};
+// Units alternate between the two query blocks, so that neighbouring units
+// are independent: 0-7 running max over four scores (block u%2, scores
+// 4(u/2)..+3); 8 the exchange with the other lane half and the new max of
+// both blocks; 9 the exponent offset -m * scale * log2(e) of both blocks;
+// 10-57 per block 8 x (two exponentials, one pack-and-sum) for score pairs
+// (block (u-10)%2); 58 the rescale factor and the sums' rescale of both
+// blocks.
+constexpr int kUnits = 59;
+constexpr int kSlotFirstUnit[33] = {0,  3,  6,  8,  9,  10, 12, 14, 16, 17, 19, 21, 23, 25, 27, 28, 30,
+                                    32, 34, 36, 38, 40, 41, 43, 45, 47, 49, 51, 52, 54, 56, 58, 59};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -388,10 +392,11 @@ __device__ __forceinline__ void pin(const T& x) {
 }
 
 struct SoftmaxState {
-  float mx[kNB];   // partial max of the tile's scores
-  float neg[kNB];  // -m * scale * log2(e)
-  float rs[kNB];   // fp32 sum of this tile's probabilities
-  float rsb[kNB];  // sum of the bf16-rounded probabilities
+  float mx[kNB];     // partial max of the tile's scores
+  float m_new[kNB];  // the max after this tile (lazily moved)
+  float neg[kNB];    // -m * scale * log2(e)
+  float rs[kNB];     // fp32 sum of this tile's probabilities
+  float rsb[kNB];    // sum of the bf16-rounded probabilities
   bf16x2 pp[kNB][8];
 };
 
@@ -399,7 +404,7 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxSta
                                              float (&l_run)[kNB], float (&lb_run)[kNB], float (&alpha)[kNB],
                                              float sl2) {
   if (u < 8) {
-    const int b = u >> 2, q = (u & 3) * 4;
+    const int b = u & 1, q = (u >> 1) * 4;
     if (q == 0) {
       st.mx[b] = __builtin_fmaxf(__builtin_fmaxf(s[b][0], s[b][1]), __builtin_fmaxf(s[b][2], s[b][3]));
     } else {
@@ -407,24 +412,36 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxSta
                                  __builtin_fmaxf(s[b][q + 1], __builtin_fmaxf(s[b][q + 2], s[b][q + 3])));
     }
     pin(st.mx[b]);
-  } else if (u < 10) {
+  } else if (u == 8) {
     // Both lane halves hold disjoint keys of the same query and agree on the
-    // max after the exchange.
-    const int b = u - 8;
-    const float mx = xmax32(st.mx[b]);
-    const float m_new = __builtin_fmaxf(m_run[b], mx);
-    const bool grow = (m_new - m_run[b]) * sl2 > kLazyRescaleLog2;
-    const float m_upd = grow ? m_new : m_run[b];
-    alpha[b] = (m_upd == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run[b] - m_upd) * sl2);
-    m_run[b] = m_upd;
-    l_run[b] *= alpha[b];
-    lb_run[b] *= alpha[b];
-    st.neg[b] = (m_upd == -INFINITY) ? 0.f : -m_upd * sl2;
-    st.rs[b] = 0.f;
-    st.rsb[b] = 0.f;
-    pin(st.neg[b]);
+    // max after the exchange.  The max moves only when it grows by more than
+    // 2^8 in the exponent.
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+      const float mx = xmax32(st.mx[b]);
+      const float m_new = __builtin_fmaxf(m_run[b], mx);
+      const bool grow = (m_new - m_run[b]) * sl2 > kLazyRescaleLog2;
+      st.m_new[b] = grow ? m_new : m_run[b];
+      pin(st.m_new[b]);
+    }
+  } else if (u == 9) {
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+      st.neg[b] = (st.m_new[b] == -INFINITY) ? 0.f : -st.m_new[b] * sl2;
+      st.rs[b] = 0.f;
+      st.rsb[b] = 0.f;
+      pin(st.neg[b]);
+    }
+  } else if (u == 58) {
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+      alpha[b] = (st.m_new[b] == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run[b] - st.m_new[b]) * sl2);
+      m_run[b] = st.m_new[b];
+      l_run[b] *= alpha[b];
+      lb_run[b] *= alpha[b];
+    }
   } else {
-    const int e = u - 10, b = e / 24, r = e % 24, t = r / 3, kind = r % 3;
+    const int e = u - 10, b = e & 1, r = e >> 1, t = r / 3, kind = r % 3;
     if (kind < 2) {
       const int i = 2 * t + kind;
       const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], sl2, st.neg[b]));
