@@ -18,6 +18,9 @@ Serving") defines:
   2C, split into 2C contiguous chunks, rank k holds chunks k and 2C-1-k) and
   the remaining-attention workload W(R, P) = RP + R(R+1)/2 (Sec. 2.2,
   equation "remaining-attention").
+* ``cache``      -- the KV-cache steps after the attention: writing a
+  request's new K/V into the block-16 paged cache (Sec. 2.2, 7.1, 8) and
+  re-sharding rows between CP degrees (Sec. 6.2, 7.2).
 * ``brute``      -- scalar-loop restatement used only to pin ``attention``
   on tiny inputs.
 

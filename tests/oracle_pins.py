@@ -213,3 +213,80 @@ def check_plan(shard_plan, remaining_workload, shard_plan_fast=None):
                 assert shard_plan_fast(P, R, C, r) == plan
         assert total == remaining_workload(R, P), "sum over ranks != W(R, P)"
         assert sorted(seen) == list(range(P, P + R)), "rows are not a bijection onto the suffix"
+
+
+def check_writeback(write_paged, rank_writeback, gather_paged, seed=9):
+    """Write-back into the paged cache (Sec. 2.2, 7.1, 8): the addressing by
+    hand, the round trip through the prefix gather (itself pinned by
+    ``check_paged_prefix``), every new token written exactly once by the CP
+    ranks together, and nothing else touched."""
+    # Addressing worked out by hand: position p -> block table[p // 16], slot p % 16.
+    table = [4, 0, 2]
+    cache = np.zeros((5, 16, 1, 1))
+    out = write_paged(cache, table, [0, 17, 37], np.array([[[1.0]], [[2.0]], [[3.0]]]))
+    assert out[4, 0, 0, 0] == 1.0 and out[0, 1, 0, 0] == 2.0 and out[2, 5, 0, 0] == 3.0, "block/slot addressing"
+    assert np.count_nonzero(out) == 3, "write touched other slots"
+    assert np.count_nonzero(cache) == 0, "write must not modify its input"
+    rng = _rng(seed)
+    Hkv, D, B = 2, 4, 16
+    for P, R, C in [(32, 45, 2), (0, 70, 4), (16, 9, 3), (48, 3, 2), (0, 16, 1)]:
+        L = P + R
+        nb = -(-L // B)
+        spare = 2
+        table = rng.permutation(nb + spare)[:nb]
+        x = rng.standard_normal((L, Hkv, D))
+        cache = np.full((nb + spare, B, Hkv, D), np.nan)
+        cache = write_paged(cache, table, list(range(P)), x[:P])          # the cached prefix
+        before = cache.copy()
+        for r in range(C):
+            s = -(-R // (2 * C))
+            rows = []
+            for chunk in (r, 2 * C - 1 - r):                                # zigzag rows by hand
+                lo, hi = P + chunk * s, min(P + (chunk + 1) * s, L)
+                rows.extend(range(lo, max(lo, hi)))
+            cache = rank_writeback(cache, table, P, R, C, r, x[rows] if rows else x[:0])
+        assert np.array_equal(gather_paged(cache, table, L), x), "write-back does not round-trip"
+        for pos in range(P):
+            b, t = table[pos // B], pos % B
+            assert np.array_equal(cache[b, t], before[b, t]), "prefix slots rewritten"
+        used = {(int(table[p // B]), p % B) for p in range(L)}
+        for b in range(nb + spare):
+            for t in range(B):
+                if (b, t) not in used:
+                    assert np.isnan(cache[b, t]).all(), "slot outside the request written"
+
+
+def check_repartition(repartition, seed=10):
+    """Re-sharding rows between CP degrees (Sec. 6.2, 7.2): every destination
+    row is the row of its global position (zigzag rows worked out by hand);
+    C -> C is the identity and C -> 2C -> C a round trip; when 4C divides the
+    padded length, degree-2C ranks 2k and 2k+1 draw only on degree-C rank k."""
+    rng = _rng(seed)
+
+    def rows_of(P, R, C, r):
+        s = -(-R // (2 * C))
+        out = []
+        for chunk in (r, 2 * C - 1 - r):
+            lo, hi = P + chunk * s, min(P + (chunk + 1) * s, P + R)
+            out.extend(range(lo, max(lo, hi)))
+        return out
+
+    for P, R, C_src, C_dst in [(0, 64, 2, 4), (16, 37, 4, 2), (0, 70, 3, 5), (32, 8, 1, 4), (0, 128, 4, 8),
+                               (0, 5, 4, 1)]:
+        x = rng.standard_normal((R, 3))
+        src = [x[np.array(rows_of(P, R, C_src, r), dtype=np.int64) - P] for r in range(C_src)]
+        dst = repartition(P, R, C_src, src, C_dst)
+        assert len(dst) == C_dst
+        for r in range(C_dst):
+            want = x[np.array(rows_of(P, R, C_dst, r), dtype=np.int64) - P]
+            assert np.array_equal(np.asarray(dst[r]).reshape(want.shape), want), "row of the wrong position"
+        same = repartition(P, R, C_src, src, C_src)
+        assert all(np.array_equal(a, b) for a, b in zip(same, src)), "C -> C is not the identity"
+        back = repartition(P, R, C_dst, dst, C_src)
+        assert all(np.array_equal(np.asarray(a).reshape(b.shape), b) for a, b in zip(back, src)), "round trip"
+    # Pairwise locality: tag each row with its source rank.
+    for C, R in [(2, 64), (4, 256), (1, 8)]:
+        tags = [np.full((len(rows_of(0, R, C, r)), 1), float(r)) for r in range(C)]
+        dst = repartition(0, R, C, tags, 2 * C)
+        for r2 in range(2 * C):
+            assert (np.asarray(dst[r2]) == r2 // 2).all(), "degree-2C rank 2k+j must come from rank k"

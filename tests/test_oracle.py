@@ -7,6 +7,7 @@ import pytest
 
 import oracle
 from oracle import attention as oatt
+from oracle import cache as ocache
 from oracle import plan as oplan
 import oracle_pins as pins
 
@@ -123,3 +124,11 @@ def test_plan_rejects_bad_arguments():
     for args in [(0, 10, 0, 0), (0, 10, 2, 2), (0, 10, 2, -1), (-16, 10, 2, 0)]:
         with pytest.raises(ValueError):
             oplan.shard_plan_fast(*args)
+
+
+def test_paged_writeback_round_trip():
+    pins.check_writeback(ocache.write_paged, ocache.rank_writeback, oatt.gather_paged)
+
+
+def test_repartition_between_degrees():
+    pins.check_repartition(ocache.repartition)

@@ -26,8 +26,12 @@ def _mutant(filename, old, new):
     return mod
 
 
-def _all_pins(att, plan):
+def _all_pins(att, plan, cache=None):
+    if cache is None:
+        from oracle import cache
     checks = [
+        lambda: pins.check_writeback(cache.write_paged, cache.rank_writeback, att.gather_paged),
+        lambda: pins.check_repartition(cache.repartition),
         lambda: pins.check_brute(att.attend),
         lambda: pins.check_sdpa(att.full_causal_attention),
         lambda: pins.check_closed_forms(att.full_causal_attention),
@@ -67,6 +71,26 @@ PLAN_MUTATIONS = [
     ("W drops the prefix term", "return R * P + R * (R + 1) // 2", "return R * (R + 1) // 2"),
     ("diagonal not counted", "for _key in range(pos + 1):", "for _key in range(pos):"),
 ]
+
+
+CACHE_MUTATIONS = [
+    ("slot off by one", "out[table[int(p) // block_tokens], int(p) % block_tokens] = rows[i]",
+     "out[table[int(p) // block_tokens], (int(p) + 1) % block_tokens] = rows[i]"),
+    ("write-back ignores the block table", "out[table[int(p) // block_tokens], int(p) % block_tokens] = rows[i]",
+     "out[int(p) // block_tokens, int(p) % block_tokens] = rows[i]"),
+    ("write-back uses the first chunk only", "return write_paged(cache, block_table, plan[\"row_pos\"], rank_rows, block_tokens)",
+     "return write_paged(cache, block_table, plan[\"row_pos\"][:plan[\"chunks\"][0][2]], rank_rows[:plan[\"chunks\"][0][2]], block_tokens)"),
+    ("repartition reads the destination's own plan", "plan = shard_plan_fast(P, R, C_src, r)",
+     "plan = shard_plan_fast(P, R, C_dst, r) if r < C_dst else shard_plan_fast(P, R, C_src, r)"),
+    ("repartition reverses a rank's rows", "where[pos] = (r, t)", "where[pos] = (r, plan[\"n_rows\"] - 1 - t)"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", CACHE_MUTATIONS, ids=[m[0] for m in CACHE_MUTATIONS])
+def test_cache_mutation_is_caught(name, old, new):
+    from oracle import attention, plan
+    cache = _mutant("cache.py", old, new)
+    assert _all_pins(attention, plan, cache) >= 1, f"no pin catches: {name}"
 
 
 @pytest.mark.parametrize("name,old,new", ATTENTION_MUTATIONS, ids=[m[0] for m in ATTENTION_MUTATIONS])
