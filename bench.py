@@ -186,6 +186,48 @@ def main():
     attn_tflops = flop / (attn_ms * 1e-3) / 1e12
     value = flop / (ms_step * 1e-3) / 1e12
 
+    # --- the KV-cache steps after the attention (not part of the timed step) --
+    def timed(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    # All C ranks of the request, as one GPU per rank would each do for its own.
+    rank_rows = [torch.as_tensor(cp.shard_plan(P, R, C, r)[1] - P, device=dev) for r in range(C)]
+    plans = [cp.shard_plan(P, R, C, r)[0] for r in range(C)]
+    k_ranks = [k[ix].contiguous() for ix in rank_rows]
+    v_ranks = [v[ix].contiguous() for ix in rank_rows]
+    n_req_blocks = -(-(P + R) // synth.BLOCK_TOKENS)
+    wb_table = torch.randperm(n_req_blocks, generator=gen, device="cuda").to(torch.int32)
+    k_store = torch.empty((n_req_blocks, synth.BLOCK_TOKENS, Hkv, D), dtype=torch.bfloat16, device=dev)
+    v_store = torch.empty_like(k_store)
+
+    def writeback():
+        for r in range(C):
+            cp.kv_writeback(plans[r], k_ranks[r], v_ranks[r], k_store, v_store, wb_table, stream=stream)
+
+    wb_ms = timed(writeback)
+    wb_bytes = 2 * 2 * R * Hkv * D * 2                # K and V rows, read once and written once
+    dst_plans = [cp.shard_plan(P, R, 2 * C, r)[0] for r in range(2 * C)]
+    dst_k = [torch.empty((pl.n_rows, Hkv, D), dtype=torch.bfloat16, device=dev) for pl in dst_plans]
+    dst_v = [torch.empty_like(t) for t in dst_k]
+
+    def reshard():
+        for r in range(2 * C):
+            cp.repartition(P, R, k_ranks, 2 * C, r, dst_k[r], stream=stream)
+            cp.repartition(P, R, v_ranks, 2 * C, r, dst_v[r], stream=stream)
+
+    rp_ms = timed(reshard)
+    rp_bytes = 2 * 2 * R * Hkv * D * 2                # K and V rows, read once and written once
+    del k_ranks, v_ranks, dst_k, dst_v, k_store, v_store
+
     # --- CPU oracle on a bounded sample of the same rows ----------------------
     cpu = None
     parity = None
@@ -227,6 +269,18 @@ def main():
             "kernel": "lse_merge_kernel", "bound": "hbm", "ms": round(merge_ms, 4),
             "bytes": merge_bytes, "GB_s": round(merge_gbs, 1),
             "frac": round(merge_gbs / PEAK_HBM_GBS, 4),
+        },
+        "kv_writeback": {
+            "kernel": "kv_writeback_kernel", "bound": "hbm", "ms": round(wb_ms, 4), "bytes": wb_bytes,
+            "GB_s": round(wb_bytes / (wb_ms * 1e-3) / 1e9, 1),
+            "frac": round(wb_bytes / (wb_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "what": "every rank's new K and V rows into the block-16 paged cache (C launches)",
+        },
+        "repartition": {
+            "kernel": "repartition_kernel", "bound": "hbm", "ms": round(rp_ms, 4), "bytes": rp_bytes,
+            "GB_s": round(rp_bytes / (rp_ms * 1e-3) / 1e9, 1),
+            "frac": round(rp_bytes / (rp_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "what": "the request's K and V rows re-sharded from degree C to degree 2C (4C launches)",
         },
         "cpu_baseline": cpu,
         "parity_sample": parity,

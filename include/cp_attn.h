@@ -13,6 +13,9 @@
  *             are computed, attending to the P cached keys and to the earlier
  *             uncached ones; the work is W(R,P) = RP + R(R+1)/2 pairs.
  *   Sec. 7.1  The cached prefix is a sequence of fixed-size cache blocks.
+ *   Sec. 6.2, 7.2  After a worker split or merge, and for replication between
+ *             workers of different CP degree, resident KV is re-sharded to
+ *             the destination's CP geometry.
  *
  * Conventions shared by every call:
  *   - Tensors are dense, row-major, in device memory unless a pointer is
@@ -56,6 +59,7 @@ extern "C" {
 #define CP_HEAD_DIM 128
 #define CP_KV_BLOCK_TOKENS 16
 #define CP_MAX_MERGE_PARTS 16
+#define CP_MAX_DEGREE 64        /* largest C of cp_repartition */
 
 /* kv_rank values of cp_partial_desc besides a rank number 0..C-1. */
 #define CP_KV_ALL (-1)  /* every causally visible suffix key (all-gathered KV) */
@@ -207,6 +211,55 @@ int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_hea
 int cp_attn_merge(int32_t n_parts, const float* const* o_parts, const float* const* lse_parts,
                   int64_t n_tokens, int32_t n_heads, int32_t head_dim, void* o_out,
                   int32_t out_bf16, float* lse_out, const cp_rank_plan* restore, void* stream);
+
+/*
+ * Paged KV write-back: stores one CP rank's new K and V rows in the block-16
+ * paged cache, where a later request's prefix hit reads them (Sec. 2.2:
+ * prefill builds the KV states of its tokens and prefix caching keeps them
+ * for later requests; Sec. 7.1: one trie node is one cache block; Sec. 8: the
+ * destination installs KV states in physical blocks it reserved).
+ *   plan        the rank's plan, as from cp_shard_plan (checked against it);
+ *               plan->prefix_len must be a multiple of 16, so that new
+ *               tokens never land in a block of the (shared) cached prefix.
+ *   k_rows, v_rows  bf16 device [plan->n_rows][n_heads_kv][head_dim]: the
+ *               rank's rows in plan order (row t is global position
+ *               row_pos[t]).  16-byte aligned.
+ *   n_heads_kv, head_dim  Hkv >= 1; head_dim a multiple of 8.
+ *   k_cache, v_cache  bf16 device [n_blocks][16][n_heads_kv][head_dim].
+ *   block_table int32 device [table_len]: physical block of each logical
+ *               block of the request; position p goes to block
+ *               block_table[p / 16], slot p % 16.  table_len must cover
+ *               the request: table_len >= ceil((P + R) / 16).
+ * Entries outside [0, n_blocks) are skipped on the device (nothing is
+ * written for those rows); the ranks of one request write disjoint slots.
+ * Errors: CP_ERR_INVALID (plan, pointers, alignment, prefix_len % 16,
+ * table_len, shapes), CP_ERR_HIP.
+ */
+int cp_kv_writeback(const cp_rank_plan* plan, const void* k_rows, const void* v_rows,
+                    int32_t n_heads_kv, int32_t head_dim, void* k_cache, void* v_cache,
+                    int64_t n_blocks, const int32_t* block_table, int64_t table_len, void* stream);
+
+/*
+ * Re-shards one request's per-rank rows from CP degree C_src to degree C_dst
+ * (Sec. 6.2: after a split or merge, resident KV is installed under the new
+ * CP geometry; Sec. 7.2: inter-degree replication repartitions KV states for
+ * the destination worker).  Row t of destination rank dst_rank (plan
+ * cp_shard_plan(P, R, C_dst, dst_rank)) receives the row of the same global
+ * position from the degree-C_src rank that holds it.  When 4C divides the
+ * padded suffix, going between degrees C and 2C is pairwise: degree-2C ranks
+ * 2k and 2k+1 draw only on degree-C rank k, and rank k only on them.
+ *   src_rows    host array of C_src device pointers: rank r's rows
+ *               [n_rows_r][row_bytes] in its plan order (NULL allowed for a
+ *               rank with no rows).  16-byte aligned.
+ *   dst_rows    device [n_rows_dst][row_bytes]; must not overlap a source.
+ *   row_bytes   bytes per row, a positive multiple of 16 (K or V rows:
+ *               Hkv * D * 2).
+ *   1 <= C_src, C_dst <= CP_MAX_DEGREE, 0 <= dst_rank < C_dst.
+ * Errors: CP_ERR_INVALID, CP_ERR_UNSUPPORTED (positions beyond 2^31),
+ * CP_ERR_HIP.
+ */
+int cp_repartition(int64_t P, int64_t R, int32_t C_src, const void* const* src_rows, int32_t C_dst,
+                   int32_t dst_rank, void* dst_rows, int64_t row_bytes, void* stream);
 
 #ifdef __cplusplus
 }

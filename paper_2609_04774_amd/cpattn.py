@@ -26,9 +26,11 @@ CP_KV_BLOCK_TOKENS = 16
 CP_MAX_MERGE_PARTS = 16
 CP_KV_ALL = -1
 CP_KV_NONE = -2
+CP_MAX_DEGREE = 64
 
 EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
-            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_merge")
+            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_merge",
+            "cp_kv_writeback", "cp_repartition")
 
 
 class CpChunk(ctypes.Structure):
@@ -99,6 +101,14 @@ def _load():
                                   ctypes.POINTER(ctypes.c_void_p), ctypes.c_int64, ctypes.c_int32,
                                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                   ctypes.POINTER(CpRankPlan), ctypes.c_void_p]
+    lib.cp_kv_writeback.restype = ctypes.c_int
+    lib.cp_kv_writeback.argtypes = [ctypes.POINTER(CpRankPlan), ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.cp_repartition.restype = ctypes.c_int
+    lib.cp_repartition.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                   ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     return lib
 
 
@@ -226,3 +236,23 @@ def attn_merge(o_parts, lse_parts, o_out, lse_out=None, restore: Optional[CpRank
 
 def default_scale(head_dim: int = CP_HEAD_DIM) -> float:
     return 1.0 / math.sqrt(head_dim)
+
+
+def kv_writeback(plan: CpRankPlan, k_rows, v_rows, k_cache, v_cache, block_table, stream=None):
+    """cp_kv_writeback of torch device tensors: the rank's rows [n_rows, Hkv, D]
+    (plan order) into caches [n_blocks, 16, Hkv, D] through block_table."""
+    n_blocks, _, Hkv, D = k_cache.shape
+    _check(lib.cp_kv_writeback(ctypes.byref(plan), _ptr(k_rows), _ptr(v_rows), Hkv, D, _ptr(k_cache),
+                               _ptr(v_cache), n_blocks, _ptr(block_table), block_table.numel(),
+                               _stream_handle(stream)))
+
+
+def repartition(prefix_len: int, new_len: int, src_rows, C_dst: int, dst_rank: int, dst_rows, stream=None):
+    """cp_repartition of torch device tensors: src_rows is the list of the C_src
+    ranks' row tensors (plan order); dst_rows receives rank dst_rank's rows at
+    degree C_dst.  A row is everything after a tensor's first dimension."""
+    C_src = len(src_rows)
+    ptrs = (ctypes.c_void_p * max(1, C_src))(*[_ptr(t) if t.numel() else None for t in src_rows])
+    row_bytes = math.prod(dst_rows.shape[1:]) * dst_rows.element_size()
+    _check(lib.cp_repartition(prefix_len, new_len, C_src, ptrs, C_dst, dst_rank, _ptr(dst_rows), row_bytes,
+                              _stream_handle(stream)))

@@ -96,4 +96,36 @@ struct MergeParams {
 
 int launch_merge(const MergeParams& p, void* stream);
 
+// ---------------------------------------------------------------------------
+// KV-cache steps after the attention: paged write-back and re-sharding.
+
+struct WritebackParams {
+  const unsigned char* k_rows;  // [n_rows][row_bytes]
+  const unsigned char* v_rows;
+  unsigned char* k_cache;       // [n_blocks][16][row_bytes]
+  unsigned char* v_cache;
+  const int32_t* block_table;
+  int64_t n_blocks;
+  int64_t row_bytes;            // Hkv * D * 2, a multiple of 16
+  int64_t q_begin[2];           // global position of each chunk's first row
+  int64_t q_len[2];             // rows of each chunk (chunk 0's rows come first)
+  int64_t n_rows;
+};
+
+int launch_writeback(const WritebackParams& p, void* stream);
+
+struct RepartitionParams {
+  const unsigned char* src[CP_MAX_DEGREE];  // source rank r's rows
+  unsigned char* dst;
+  int64_t row_bytes;
+  int64_t P, R;
+  int64_t s_src;                // chunk length at the source degree
+  int32_t C_src;
+  int64_t dst_q_begin[2];       // the destination rank's chunks (global positions)
+  int64_t dst_q_len[2];
+  int64_t n_rows;
+};
+
+int launch_repartition(const RepartitionParams& p, void* stream);
+
 }  // namespace cpattn

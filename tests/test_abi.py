@@ -217,3 +217,50 @@ def test_merge_argument_errors():
     assert _merge_status(n_tokens=5, restore=plan) == cp.CP_ERR_INVALID   # n_rows is 4
     plan.chunk[0].q_len = 2
     assert _merge_status(n_tokens=4, restore=plan) == cp.CP_ERR_INVALID   # tampered plan
+
+
+def _wb_status(P=32, R=40, C=2, rank=0, Hkv=2, D=128, rows=FAKE, cache=FAKE * 2, table=FAKE * 3,
+               table_len=None, n_blocks=8, plan=None):
+    if plan is None:
+        plan, _ = cp.shard_plan(P, R, C, rank, with_rows=False)
+    if table_len is None:
+        table_len = -(-(P + R) // 16)
+    return cp.lib.cp_kv_writeback(ctypes.byref(plan), rows, rows, Hkv, D, cache, cache, n_blocks, table,
+                                  table_len, None)
+
+
+def test_writeback_argument_errors():
+    assert _wb_status(P=40) == cp.CP_ERR_INVALID                      # prefix not block aligned
+    assert _wb_status(table_len=4) == cp.CP_ERR_INVALID               # 72 tokens need 5 blocks
+    assert _wb_status(rows=None) == cp.CP_ERR_INVALID
+    assert _wb_status(cache=FAKE + 8) == cp.CP_ERR_INVALID
+    assert _wb_status(table=FAKE + 2) == cp.CP_ERR_INVALID
+    assert _wb_status(Hkv=0) == cp.CP_ERR_INVALID
+    assert _wb_status(D=12) == cp.CP_ERR_INVALID
+    assert _wb_status(n_blocks=-1) == cp.CP_ERR_INVALID
+    plan, _ = cp.shard_plan(32, 40, 2, 0, with_rows=False)
+    plan.n_rows += 1
+    assert _wb_status(plan=plan) == cp.CP_ERR_INVALID                  # tampered plan
+    assert cp.lib.cp_kv_writeback(None, FAKE, FAKE, 2, 128, FAKE, FAKE, 8, FAKE, 5, None) == cp.CP_ERR_INVALID
+    assert cp.last_error() != ""
+
+
+def _rp_status(P=0, R=64, C_src=2, C_dst=4, dst_rank=0, src=None, dst=FAKE, row_bytes=4096):
+    ptrs = (ctypes.c_void_p * max(1, C_src))(*([FAKE * 2] * C_src if src is None else src))
+    return cp.lib.cp_repartition(P, R, C_src, ptrs, C_dst, dst_rank, dst, row_bytes, None)
+
+
+def test_repartition_argument_errors():
+    assert _rp_status(C_src=0) == cp.CP_ERR_INVALID
+    assert _rp_status(C_dst=65) == cp.CP_ERR_INVALID
+    assert _rp_status(dst_rank=4) == cp.CP_ERR_INVALID
+    assert _rp_status(dst_rank=-1) == cp.CP_ERR_INVALID
+    assert _rp_status(row_bytes=24) == cp.CP_ERR_INVALID
+    assert _rp_status(row_bytes=0) == cp.CP_ERR_INVALID
+    assert _rp_status(dst=None) == cp.CP_ERR_INVALID
+    assert _rp_status(dst=FAKE + 8) == cp.CP_ERR_INVALID
+    assert _rp_status(src=[FAKE * 2, None]) == cp.CP_ERR_INVALID      # rank 1 has rows
+    assert _rp_status(src=[FAKE * 2, FAKE + 4]) == cp.CP_ERR_INVALID
+    assert _rp_status(P=-1) == cp.CP_ERR_INVALID
+    assert _rp_status(P=1 << 31, R=64) == cp.CP_ERR_UNSUPPORTED
+    assert cp.last_error() != ""
