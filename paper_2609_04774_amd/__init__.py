@@ -2,15 +2,17 @@
 
 ``paper_2609_04774_amd.cpattn`` is the Python binding of libcpattn (the C ABI
 in include/cp_attn.h over hand-written gfx950 HIP kernels);
-``paper_2609_04774_amd.build`` compiles that library in-tree.  The binding is
+``paper_2609_04774_amd.build`` compiles that library in-tree;
+``paper_2609_04774_amd.calibrate`` fits the attention term of the paper's
+prefill-time model (Sec. 3.2) to measured kernel times.  Submodules are
 imported on first use, so building works before the library exists.
 """
 
-__all__ = ["cpattn", "build"]
+__all__ = ["cpattn", "build", "calibrate"]
 
 
 def __getattr__(name):
-    if name in ("cpattn", "build"):
+    if name in ("cpattn", "build", "calibrate"):
         import importlib
         return importlib.import_module(f"{__name__}.{name}")
     raise AttributeError(name)
