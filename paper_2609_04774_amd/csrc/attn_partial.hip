@@ -52,7 +52,6 @@ constexpr int kNB = 2;                       // blocks of 32 rows per wave
 constexpr int kTileKeys = 32;
 constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
 constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
-constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 constexpr int kRowBytes = kHeadDim * 2;
 constexpr int kTileBytes = kTileKeys * kRowBytes;
 
@@ -203,11 +202,19 @@ __device__ __forceinline__ void issue_tile(const TileLoad& t) {
   for (int q = 0; q < 4; ++q) issue_load(t, q);
 }
 
+// max(a, b, c) in one v_maximum3_f32 (NaN-propagating maximum).  fmaxf on
+// values the compiler cannot prove canonical -- the scores come out of
+// inline assembly -- would cost an extra canonicalising max per operand.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
 __device__ __forceinline__ float xmax32(float x) {
   // Max with the lane 32 apart (the other half of the same query's keys).
   auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
                                             false, false);
-  return __builtin_fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+  return __builtin_elementwise_maximum(__builtin_bit_cast(float, (unsigned)r[0]),
+                                      __builtin_bit_cast(float, (unsigned)r[1]));
 }
 
 __device__ __forceinline__ float xsum32(float x) {
@@ -220,6 +227,13 @@ __device__ __forceinline__ float xsum32(float x) {
 // (per wave); until then probabilities are taken against the stale max and
 // stay below 256, which bf16 and the fp32 sums hold exactly as well.
 constexpr float kLazyRescaleLog2 = 8.f;
+// The running max is kept in units of the exponent (score * scale * log2 e)
+// and starts at a finite "nothing seen" value far below any real score's:
+// the first tile with a visible key then always moves it, a fully masked
+// tile (scores -inf) yields probabilities exp2(-inf) = 0 against it, and no
+// lane needs a -inf special case.
+constexpr float kNoMax = -1e30f;
+constexpr float kLn2 = 0.69314718055994531f;
 
 // Per-lane LDS byte offsets of the fragments, relative to a K or V tile.
 //   K (A operand of S^T = K Q^T): lane reads tile row l32, logical chunk
@@ -283,10 +297,22 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
   mfma_result_wait();
 }
 
+// The all-ones A operand: an MFMA of it against P^T adds every query's sum of
+// its bf16 probabilities (over the k-step's 16 keys) to all 32 rows of the
+// accumulator.  The matrix cores have slack and the vector ALUs do not.
+__device__ __forceinline__ bf16x8 ones_frag() {
+  return __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
+}
+
 // O^T += V^T P^T for one 32-key tile (the last one); each V fragment serves
-// both query blocks.
+// both query blocks.  lsum gets the tile's bf16 row sums.
 __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
-                                        f32x16 (&o)[4][kNB]) {
+                                        f32x16 (&o)[4][kNB], f32x16 (&lsum)[kNB]) {
+  const bf16x8 ones = ones_frag();
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) lsum[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[b][ks], lsum[b], 0, 0, 0);
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
@@ -329,42 +355,48 @@ __device__ __forceinline__ bool tile_limits(const Tile& x, int q0, bool wave_act
   return !live || (x.t0 + kTileKeys > x.hi) || (x.t0 + kTileKeys - 1 > wave_lo);
 }
 
-// O *= alpha (per query column), in place in the accumulation registers, for
-// the rare softmax that moved the running max.  Each element goes through a
-// VGPR inside one asm statement so that O keeps living in AGPRs (a VALU
-// multiply in plain code would make the compiler move all of O to VGPRs and
-// back on every iteration).  The s_nop blocks keep the matrix-core hazards:
-// the last MFMA's results land before they are read, and the writes before
-// the next MFMA reads them.
-__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alpha)[kNB]) {
+// O and the bf16 row sums *= alpha (per query column), in place in the
+// accumulation registers, for the rare softmax that moved the running max.
+// Each element goes through a VGPR inside one asm statement so that the
+// accumulators keep living in AGPRs (a VALU multiply in plain code would make
+// the compiler move all of O to VGPRs and back on every iteration).  The
+// s_nop blocks keep the matrix-core hazards: the last MFMA's results land
+// before they are read, and the writes before the next MFMA reads them.
+__device__ __forceinline__ void scale_acc(f32x16& a, float alpha) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float x = a[r];
+    float t;
+    asm volatile(
+        "v_accvgpr_read_b32 %1, %0\n\t"
+        "v_mul_f32 %1, %1, %2\n\t"
+        "v_accvgpr_write_b32 %0, %1"
+        : "+a"(x), "=&v"(t)
+        : "v"(alpha));
+    a[r] = x;
+  }
+}
+
+__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], f32x16 (&lsum)[kNB], const float (&alpha)[kNB]) {
   bool any = false;
 #pragma unroll
   for (int b = 0; b < kNB; ++b) any |= alpha[b] != 1.f;
   if (__any(any)) {
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4");
 #pragma unroll
-    for (int b = 0; b < kNB; ++b)
+    for (int b = 0; b < kNB; ++b) {
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = o[db][b][r];
-          float t;
-          asm volatile(
-              "v_accvgpr_read_b32 %1, %0\n\t"
-              "v_mul_f32 %1, %1, %2\n\t"
-              "v_accvgpr_write_b32 %0, %1"
-              : "+a"(x), "=&v"(t)
-              : "v"(alpha[b]));
-          o[db][b][r] = x;
-        }
+      for (int db = 0; db < 4; ++db) scale_acc(o[db][b], alpha[b]);
+      scale_acc(lsum[b], alpha[b]);
+    }
     asm volatile("s_nop 7");
   }
 }
 
-// One iteration's matrix and vector work as a fixed sequence of 32 MFMA
+// One iteration's matrix and vector work as a fixed sequence of 36 MFMA
 // slots: slots 0-15 compute S_{j+1} = K_{j+1} Q^T (K step d = slot/2 feeds
-// both query blocks), slots 16-31 add P_{j-1} V_{j-1} (V fragment slot/2 - 8).
+// both query blocks), slots 16-31 add P_{j-1} V_{j-1} (V fragment slot/2 - 8),
+// slots 32-35 add P_{j-1}'s bf16 row sums (k-step (slot-32)/2).
 // The softmax of S_j is cut into units of roughly equal VALU time and dealt
 // out over the slots, so that every MFMA has vector work to overlap with;
 // LDS fragments are read three fragments (six slots) ahead, and the four
@@ -374,13 +406,15 @@ __device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alp
 // Units alternate between the two query blocks, so that neighbouring units
 // are independent: 0-7 running max over four scores (block u%2, scores
 // 4(u/2)..+3); 8 the exchange with the other lane half and the new max of
-// both blocks; 9 the exponent offset -m * scale * log2(e) of both blocks;
-// 10-57 per block 8 x (two exponentials, one pack-and-sum) for score pairs
+// both blocks (in exponent units); 9 the start of both blocks' fp32 sums;
+// 10-57 per block 8 x (two exponentials, one pack-and-fp32-sum) for score pairs
 // (block (u-10)%2); 58 the rescale factor and the sums' rescale of both
 // blocks.
 constexpr int kUnits = 59;
-constexpr int kSlotFirstUnit[33] = {0,  3,  6,  8,  9,  10, 12, 14, 16, 17, 19, 21, 23, 25, 27, 28, 30,
-                                    32, 34, 36, 38, 40, 41, 43, 45, 47, 49, 51, 52, 54, 56, 58, 59};
+constexpr int kSlots = 36;
+constexpr int kSlotFirstUnit[kSlots + 1] = {0,  3,  6,  8,  9,  10, 12, 13, 15, 16, 18, 19, 21,
+                                            23, 24, 26, 28, 29, 31, 32, 34, 36, 37, 39, 40, 42,
+                                            43, 45, 47, 48, 50, 52, 53, 55, 56, 58, 59};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -393,23 +427,19 @@ __device__ __forceinline__ void pin(const T& x) {
 
 struct SoftmaxState {
   float mx[kNB];     // partial max of the tile's scores
-  float m_new[kNB];  // the max after this tile (lazily moved)
-  float neg[kNB];    // -m * scale * log2(e)
+  float m_new[kNB];  // the max after this tile (lazily moved), exponent units
   float rs[kNB];     // fp32 sum of this tile's probabilities
-  float rsb[kNB];    // sum of the bf16-rounded probabilities
   bf16x2 pp[kNB][8];
 };
 
 __device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxState& st, float (&m_run)[kNB],
-                                             float (&l_run)[kNB], float (&lb_run)[kNB], float (&alpha)[kNB],
-                                             float sl2) {
+                                             float (&l_run)[kNB], float (&alpha)[kNB], float sl2) {
   if (u < 8) {
     const int b = u & 1, q = (u >> 1) * 4;
     if (q == 0) {
-      st.mx[b] = __builtin_fmaxf(__builtin_fmaxf(s[b][0], s[b][1]), __builtin_fmaxf(s[b][2], s[b][3]));
+      st.mx[b] = max3(__builtin_elementwise_maximum(s[b][0], s[b][1]), s[b][2], s[b][3]);
     } else {
-      st.mx[b] = __builtin_fmaxf(__builtin_fmaxf(st.mx[b], s[b][q]),
-                                 __builtin_fmaxf(s[b][q + 1], __builtin_fmaxf(s[b][q + 2], s[b][q + 3])));
+      st.mx[b] = max3(max3(st.mx[b], s[b][q], s[b][q + 1]), s[b][q + 2], s[b][q + 3]);
     }
     pin(st.mx[b]);
   } else if (u == 8) {
@@ -418,42 +448,32 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxSta
     // 2^8 in the exponent.
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
-      const float mx = xmax32(st.mx[b]);
-      const float m_new = __builtin_fmaxf(m_run[b], mx);
-      const bool grow = (m_new - m_run[b]) * sl2 > kLazyRescaleLog2;
-      st.m_new[b] = grow ? m_new : m_run[b];
+      const float mx = xmax32(st.mx[b]) * sl2;
+      st.m_new[b] = mx > m_run[b] + kLazyRescaleLog2 ? mx : m_run[b];
       pin(st.m_new[b]);
     }
   } else if (u == 9) {
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) {
-      st.neg[b] = (st.m_new[b] == -INFINITY) ? 0.f : -st.m_new[b] * sl2;
-      st.rs[b] = 0.f;
-      st.rsb[b] = 0.f;
-      pin(st.neg[b]);
-    }
+    for (int b = 0; b < kNB; ++b) st.rs[b] = -0.f;  // x + -0 is x: the first add folds away
   } else if (u == 58) {
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
-      alpha[b] = (st.m_new[b] == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run[b] - st.m_new[b]) * sl2);
+      alpha[b] = __builtin_amdgcn_exp2f(m_run[b] - st.m_new[b]);
       m_run[b] = st.m_new[b];
       l_run[b] *= alpha[b];
-      lb_run[b] *= alpha[b];
     }
   } else {
     const int e = u - 10, b = e & 1, r = e >> 1, t = r / 3, kind = r % 3;
     if (kind < 2) {
       const int i = 2 * t + kind;
-      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], sl2, st.neg[b]));
+      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], sl2, -st.m_new[b]));
       pin(x);
       s[b][i] = x;
     } else {
       const bf16x2 pp = bf16x2{(__bf16)s[b][2 * t], (__bf16)s[b][2 * t + 1]};
       st.pp[b][t] = pp;
       st.rs[b] += s[b][2 * t] + s[b][2 * t + 1];
-      st.rsb[b] = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb[b], false);
       pin(st.rs[b]);
-      pin(st.rsb[b]);
       pin(pp);
     }
   }
@@ -475,35 +495,37 @@ __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, cons
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
                                                  const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
                                                  bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB],
-                                                 f32x16 (&s_out)[kNB], float (&m_run)[kNB], float (&l_run)[kNB],
-                                                 float (&lb_run)[kNB], float (&alpha)[kNB], float sl2,
+                                                 f32x16 (&s_out)[kNB], f32x16 (&lsum)[kNB], float (&m_run)[kNB],
+                                                 float (&l_run)[kNB], float (&alpha)[kNB], float sl2,
                                                  const TileLoad& ld) {
   SoftmaxState st;
+  const bf16x8 ones = ones_frag();
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
 #pragma unroll
-  for (int slot = 0; slot < 32; ++slot) {
+  for (int slot = 0; slot < kSlots; ++slot) {
     if ((slot & 1) == 0 && slot / 2 + kLookahead < 16)
       fr[slot / 2 + kLookahead] = load_frag(slot / 2 + kLookahead, sv, sk, fo);
-    if ((slot & 7) == 1) issue_load(ld, slot >> 3);
+    if ((slot & 7) == 1 && slot < 32) issue_load(ld, slot >> 3);
     const int b = slot & 1;
     if (slot < 16) {
       const int d = slot >> 1;
       mfma_qk(s_out[b], fr[d], qf[b][d], d == 0);
-    } else {
+    } else if (slot < 32) {
       const int f = (slot >> 1) - 8;
       o[f & 3][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[8 + f], pf[b][f >> 2], o[f & 3][b], 0, 0, 0);
+    } else {
+      lsum[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[b][(slot - 32) >> 1], lsum[b], 0, 0, 0);
     }
 #pragma unroll
     for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
-      softmax_unit(u, s_in, st, m_run, l_run, lb_run, alpha, sl2);
+      softmax_unit(u, s_in, st, m_run, l_run, alpha, sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
     l_run[b] += st.rs[b];
-    lb_run[b] += st.rsb[b];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
       pf[b][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[b][4 * ks], st.pp[b][4 * ks + 1], 0, 1, 2, 3),
@@ -650,16 +672,18 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
   f32x16 o[4][kNB];
-  float m_run[kNB], l_run[kNB], lb_run[kNB];  // running max; sums of fp32 / bf16-rounded probabilities
+  f32x16 lsum[kNB];                            // sums of the bf16-rounded probabilities (every row alike)
+  float m_run[kNB], l_run[kNB];                // running max (exponent units); sum of the fp32 probabilities
+                                               // (lane's keys)
   float alpha[kNB];                            // rescale factor of the last softmax
   bf16x8 pf[kNB][2];                           // P of the previous tile
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
-    m_run[b] = -INFINITY;
+    lsum[b] = f32x16{};
+    m_run[b] = kNoMax;
     l_run[b] = 0.f;
-    lb_run[b] = 0.f;
     alpha[b] = 1.f;
     pf[b][0] = pf[b][1] = bf16x8{};
   }
@@ -683,8 +707,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     const int kn = j + 1 < n_tiles ? j + 1 : j;
     const int vp = j > 0 ? j - 1 : 0;
     pipelined_region(sv0 + (vp & (kBufs - 1)) * kTileBytes, sk0 + (kn & (kBufs - 1)) * kTileBytes, fo, qf, pf, o,
-                     s_in, s_out, m_run, l_run, lb_run, alpha, sl2, ld);
-    rescale_o(o, alpha);
+                     s_in, s_out, lsum, m_run, l_run, alpha, sl2, ld);
+    rescale_o(o, lsum, alpha);
   };
 
   // Iterations go in pairs behind one barrier.  At a pair's start every tile
@@ -701,15 +725,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0) pv_tile(sv0 + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
+  if (n_tiles > 0) pv_tile(sv0 + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, lsum);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
     const float lt = xsum32(l_run[b]);
-    const float ltb = xsum32(lb_run[b]);
-    const bool live = (m_run[b] != -INFINITY) && (lt > 0.f) && (ltb > 0.f);
+    const float ltb = lsum[b][0];  // the MFMA summed over both lane halves' keys
+    const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
     const float inv = live ? 1.f / ltb : 0.f;
     if (valid_b[b]) {
       const int64_t row = loff + qb0 + qrel_b[b];
@@ -725,7 +749,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
           v.w = o[db][b][4 * q4 + 3] * inv;
           *reinterpret_cast<float4*>(orow + db * 32 + q4 * 8 + half * 4) = v;
         }
-      if (half == 0) d.lse[row * Hq + head_b[b]] = live ? m_run[b] * p.scale + logf(lt) : -INFINITY;
+      if (half == 0) d.lse[row * Hq + head_b[b]] = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
     }
   }
 }
