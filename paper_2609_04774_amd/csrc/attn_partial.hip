@@ -47,8 +47,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;                    // wave64s per workgroup, one per SIMD
-constexpr int kNB = 2;                       // blocks of 32 rows per wave
+constexpr int kWaves = 8;                    // wave64s per workgroup, two per SIMD
+constexpr int kNB = 1;                       // blocks of 32 rows per wave
+constexpr int kGroups = 32 / kWaves / 4;     // 4-row groups of each tile one wave loads
 constexpr int kTileKeys = 32;
 constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
 constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
@@ -143,19 +144,19 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
 struct TileLoad {
   const unsigned char* kb;
   const unsigned char* vb;
-  uint32_t off[2];
-  uint32_t lk[2], lv[2];  // LDS destinations of the two row groups
+  uint32_t off[kGroups];
+  uint32_t lk[kGroups], lv[kGroups];  // LDS destinations of the row groups
 };
 
 template <int RPW>
 __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src, int kvh, int row_stride, int wave,
                                               const uint32_t (&lane_off)[RPW / 4], const int (&lane_row)[RPW / 4],
                                               const uint32_t (&lane_chunk)[RPW / 4], uint32_t sk, uint32_t sv) {
-  static_assert(RPW == 8, "two row groups of four per wave");
+  static_assert(RPW == 4 * kGroups, "row groups of four per wave");
   const int row0 = wave * RPW;
   TileLoad t;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < kGroups; ++i) {
     t.off[i] = lane_off[i];
     t.lk[i] = sk + (uint32_t)((row0 + 4 * i) * kRowBytes);
     t.lv[i] = sv + (uint32_t)((row0 + 4 * i) * kRowBytes);
@@ -179,7 +180,7 @@ __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src
     if (x.t0 + kTileKeys > x.vis) {
       const int clamp_row = x.vis - 1 - x.t0;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < kGroups; ++i) {
         const int r = lane_row[i] < clamp_row ? lane_row[i] : clamp_row;
         t.off[i] = __umul24((uint32_t)r, (uint32_t)row_stride) + lane_chunk[i];
       }
@@ -188,7 +189,7 @@ __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src
   return t;
 }
 
-// Load q (0..3) of a prepared tile: K or V rows of group q/2.
+// Load q (0 .. 2*kGroups-1) of a prepared tile: K or V rows of group q/2.
 __device__ __forceinline__ void issue_load(const TileLoad& t, int q) {
   const int i = q >> 1;
   if (q & 1)
@@ -199,7 +200,7 @@ __device__ __forceinline__ void issue_load(const TileLoad& t, int q) {
 
 __device__ __forceinline__ void issue_tile(const TileLoad& t) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) issue_load(t, q);
+  for (int q = 0; q < 2 * kGroups; ++q) issue_load(t, q);
 }
 
 // max(a, b, c) in one v_maximum3_f32 (NaN-propagating maximum).  fmaxf on
@@ -233,28 +234,29 @@ constexpr float kLazyRescaleLog2 = 8.f;
 // tile (scores -inf) yields probabilities exp2(-inf) = 0 against it, and no
 // lane needs a -inf special case.
 constexpr float kNoMax = -1e30f;
+
 constexpr float kLn2 = 0.69314718055994531f;
 
-// Per-lane LDS byte offsets of the fragments, relative to a K or V tile.
-//   K (A operand of S^T = K Q^T): lane reads tile row l32, logical chunk
-//   2ds+half; only the 8 steps ds need their own offset, computed as
-//   krow + ((2ds) ^ kx) * 16.
+// Per-lane LDS byte offsets of the fragments in buffer 0 (buffer b adds
+// b * kTileBytes: one scalar-plus-vector add per fragment and tile).
+//   K (A operand of S^T = K Q^T): for step ds the lane reads tile row l32,
+//   logical chunk 2ds+half: k[ds] = l32 * 256 + ((2ds) ^ swz(l32) ^ half) * 16.
 //   V (A operand of O^T += V^T P^T, transposed 64-bit reads): for k-step ks
 //   and head-dim block db the group's 16 lanes read rows
 //   kbase + i/4 (kbase = 16ks + 4half, +8 for the second half of the slots) at
 //   columns d0 + 4(i%4), d0 = 32db + 16(group&1).  swz of those rows does not
-//   depend on ks, so ks is a constant +4096 and 4 db x 2 halves need offsets.
+//   depend on ks, so ks is a constant +4096 and 4 db x 2 halves need offsets
+//   (these include the start of the V buffers, kBufs * kTileBytes).
 struct FragOffsets {
-  uint32_t krow;
-  uint32_t kx;
+  uint32_t k[8];
   uint32_t v[4][2];
 };
 
 __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
   FragOffsets f;
   const int l32 = lane & 31, half = lane >> 5, grp = lane >> 4, gi = lane & 15;
-  f.krow = (uint32_t)(l32 * kRowBytes);
-  f.kx = (uint32_t)(swz(l32) ^ half);
+#pragma unroll
+  for (int ds = 0; ds < 8; ++ds) f.k[ds] = (uint32_t)(l32 * kRowBytes + (((2 * ds) ^ swz(l32) ^ half) << 4));
   const int row1 = half * 4 + (gi >> 2);
   const int row2 = row1 + 8;
 #pragma unroll
@@ -262,8 +264,8 @@ __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
     const int dcol = db * 32 + (grp & 1) * 16 + 4 * (gi & 3);
     const int c = dcol >> 3;
     const int e = (dcol & 7) * 2;
-    f.v[db][0] = (uint32_t)(row1 * kRowBytes + ((c ^ swz(row1)) << 4) + e);
-    f.v[db][1] = (uint32_t)(row2 * kRowBytes + ((c ^ swz(row2)) << 4) + e);
+    f.v[db][0] = (uint32_t)(kBufs * kTileBytes + row1 * kRowBytes + ((c ^ swz(row1)) << 4) + e);
+    f.v[db][1] = (uint32_t)(kBufs * kTileBytes + row2 * kRowBytes + ((c ^ swz(row2)) << 4) + e);
   }
   return f;
 }
@@ -276,9 +278,9 @@ __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
 // 16 more MFMAs, or an explicit s_nop block, before the scores are read).
 __device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& k, const bf16x8& q, bool first) {
   if (first)
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "a"(q));
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "v"(q));
   else
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "a"(q));
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "v"(q));
 }
 
 // Wait states between the last score MFMA of the prologue and the first
@@ -290,7 +292,7 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
                                         f32x16 (&s)[kNB]) {
 #pragma unroll
   for (int ds = 0; ds < 8; ++ds) {
-    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + fo.krow + (((uint32_t)(2 * ds) ^ fo.kx) << 4));
+    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + fo.k[ds]);
 #pragma unroll
     for (int b = 0; b < kNB; ++b) mfma_qk(s[b], kf, qf[b][ds], ds == 0);
   }
@@ -329,12 +331,17 @@ __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffse
 // Masks keys at tile offsets >= lim[b]; score register r is tile key
 // (r/4)*8 + 4*half + r%4.
 __device__ __forceinline__ void mask_tile(f32x16 (&s)[kNB], int half, const int (&lim)[kNB]) {
+  // Compare the constant part of the offset with lim - 4*half, so that no
+  // per-register offsets need to be kept in registers.
+  int limh[kNB];
+#pragma unroll
+  for (int b = 0; b < kNB; ++b) limh[b] = lim[b] - half * 4;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int off = (r >> 2) * 8 + half * 4 + (r & 3);
+    const int off = (r >> 2) * 8 + (r & 3);
 #pragma unroll
     for (int b = 0; b < kNB; ++b)
-      if (off >= lim[b]) s[b][r] = -INFINITY;
+      if (off >= limh[b]) s[b][r] = -INFINITY;
   }
 }
 
@@ -355,66 +362,44 @@ __device__ __forceinline__ bool tile_limits(const Tile& x, int q0, bool wave_act
   return !live || (x.t0 + kTileKeys > x.hi) || (x.t0 + kTileKeys - 1 > wave_lo);
 }
 
-// O and the bf16 row sums *= alpha (per query column), in place in the
-// accumulation registers, for the rare softmax that moved the running max.
-// Each element goes through a VGPR inside one asm statement so that the
-// accumulators keep living in AGPRs (a VALU multiply in plain code would make
-// the compiler move all of O to VGPRs and back on every iteration).  The
-// s_nop blocks keep the matrix-core hazards: the last MFMA's results land
-// before they are read, and the writes before the next MFMA reads them.
-__device__ __forceinline__ void scale_acc(f32x16& a, float alpha) {
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    float x = a[r];
-    float t;
-    asm volatile(
-        "v_accvgpr_read_b32 %1, %0\n\t"
-        "v_mul_f32 %1, %1, %2\n\t"
-        "v_accvgpr_write_b32 %0, %1"
-        : "+a"(x), "=&v"(t)
-        : "v"(alpha));
-    a[r] = x;
-  }
-}
+// O and the bf16 row sums *= alpha (per query column), in place, for the
+// rare softmax that moved the running max.  Every register of the kernel is
+// an ordinary VGPR (two waves per SIMD leave 256 per lane, enough for all of
+// them), so this is plain vector code.
 
 __device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], f32x16 (&lsum)[kNB], const float (&alpha)[kNB]) {
   bool any = false;
 #pragma unroll
   for (int b = 0; b < kNB; ++b) any |= alpha[b] != 1.f;
   if (__any(any)) {
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4");
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
 #pragma unroll
-      for (int db = 0; db < 4; ++db) scale_acc(o[db][b], alpha[b]);
-      scale_acc(lsum[b], alpha[b]);
+      for (int db = 0; db < 4; ++db) o[db][b] *= alpha[b];
+      lsum[b] *= alpha[b];
     }
-    asm volatile("s_nop 7");
   }
 }
 
-// One iteration's matrix and vector work as a fixed sequence of 36 MFMA
-// slots: slots 0-15 compute S_{j+1} = K_{j+1} Q^T (K step d = slot/2 feeds
-// both query blocks), slots 16-31 add P_{j-1} V_{j-1} (V fragment slot/2 - 8),
-// slots 32-35 add P_{j-1}'s bf16 row sums (k-step (slot-32)/2).
-// The softmax of S_j is cut into units of roughly equal VALU time and dealt
-// out over the slots, so that every MFMA has vector work to overlap with;
-// LDS fragments are read three fragments (six slots) ahead, and the four
-// loads of tile j+5 go out at slots 1, 9, 17 and 25.  Scheduling barriers
-// keep the slots in this order.
+// One iteration's matrix and vector work as a fixed sequence of 18 MFMA
+// slots: slots 0-7 compute S_{j+1} = K_{j+1} Q^T (K step d = slot), slots
+// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8), slots 16-17 add P_{j-1}'s
+// bf16 row sums (k-step slot - 16).  The softmax of S_j is cut into units of
+// roughly equal VALU time and dealt out over the slots, so that every MFMA
+// has vector work to overlap with; LDS fragments are read three slots ahead,
+// and the two loads of tile j+5 (K rows, then V rows) go out at slots 1 and
+// 9.  Scheduling barriers keep the slots in this order.  The other wave on
+// the same SIMD runs the same sequence shifted in time, so one wave's vector
+// and scalar work issues while the other's matrix work runs.
 //
-// Units alternate between the two query blocks, so that neighbouring units
-// are independent: 0-7 running max over four scores (block u%2, scores
-// 4(u/2)..+3); 8 the exchange with the other lane half and the new max of
-// both blocks (in exponent units); 9 the start of both blocks' fp32 sums;
-// 10-57 per block 8 x (two exponentials, one pack-and-fp32-sum) for score pairs
-// (block (u-10)%2); 58 the rescale factor and the sums' rescale of both
-// blocks.
-constexpr int kUnits = 59;
-constexpr int kSlots = 36;
-constexpr int kSlotFirstUnit[kSlots + 1] = {0,  3,  6,  8,  9,  10, 12, 13, 15, 16, 18, 19, 21,
-                                            23, 24, 26, 28, 29, 31, 32, 34, 36, 37, 39, 40, 42,
-                                            43, 45, 47, 48, 50, 52, 53, 55, 56, 58, 59};
+// Units: 0-3 running max over four scores each (scores 4u..4u+3); 4 the
+// exchange with the other lane half and the new max (in exponent units),
+// and the start of the fp32 sum; 5-28 eight times (two exponentials, one
+// pack-and-fp32-sum) for score pairs; 29 the rescale factor and the sum's
+// rescale.
+constexpr int kUnits = 30;
+constexpr int kSlots = 18;
+constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 8, 10, 12, 14, 15, 17, 19, 20, 22, 24, 26, 27, 29, 30};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -426,54 +411,45 @@ __device__ __forceinline__ void pin(const T& x) {
 }
 
 struct SoftmaxState {
-  float mx[kNB];     // partial max of the tile's scores
-  float m_new[kNB];  // the max after this tile (lazily moved), exponent units
-  float rs[kNB];     // fp32 sum of this tile's probabilities
-  bf16x2 pp[kNB][8];
+  float mx;     // partial max of the tile's scores
+  float m_new;  // the max after this tile (lazily moved), exponent units
+  float rs;     // fp32 sum of this tile's probabilities
+  bf16x2 pp[8];
 };
 
-__device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxState& st, float (&m_run)[kNB],
-                                             float (&l_run)[kNB], float (&alpha)[kNB], float sl2) {
-  if (u < 8) {
-    const int b = u & 1, q = (u >> 1) * 4;
-    if (q == 0) {
-      st.mx[b] = max3(__builtin_elementwise_maximum(s[b][0], s[b][1]), s[b][2], s[b][3]);
-    } else {
-      st.mx[b] = max3(max3(st.mx[b], s[b][q], s[b][q + 1]), s[b][q + 2], s[b][q + 3]);
-    }
-    pin(st.mx[b]);
-  } else if (u == 8) {
+__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float& m_run, float& l_run,
+                                             float& alpha, float sl2) {
+  if (u < 4) {
+    const int q = 4 * u;
+    if (q == 0)
+      st.mx = max3(__builtin_elementwise_maximum(s[0], s[1]), s[2], s[3]);
+    else
+      st.mx = max3(max3(st.mx, s[q], s[q + 1]), s[q + 2], s[q + 3]);
+    pin(st.mx);
+  } else if (u == 4) {
     // Both lane halves hold disjoint keys of the same query and agree on the
     // max after the exchange.  The max moves only when it grows by more than
     // 2^8 in the exponent.
-#pragma unroll
-    for (int b = 0; b < kNB; ++b) {
-      const float mx = xmax32(st.mx[b]) * sl2;
-      st.m_new[b] = mx > m_run[b] + kLazyRescaleLog2 ? mx : m_run[b];
-      pin(st.m_new[b]);
-    }
-  } else if (u == 9) {
-#pragma unroll
-    for (int b = 0; b < kNB; ++b) st.rs[b] = -0.f;  // x + -0 is x: the first add folds away
-  } else if (u == 58) {
-#pragma unroll
-    for (int b = 0; b < kNB; ++b) {
-      alpha[b] = __builtin_amdgcn_exp2f(m_run[b] - st.m_new[b]);
-      m_run[b] = st.m_new[b];
-      l_run[b] *= alpha[b];
-    }
+    const float mx = xmax32(st.mx) * sl2;
+    st.m_new = mx > m_run + kLazyRescaleLog2 ? mx : m_run;
+    st.rs = -0.f;  // x + -0 is x: the first add folds away
+    pin(st.m_new);
+  } else if (u == kUnits - 1) {
+    alpha = __builtin_amdgcn_exp2f(m_run - st.m_new);
+    m_run = st.m_new;
+    l_run *= alpha;
   } else {
-    const int e = u - 10, b = e & 1, r = e >> 1, t = r / 3, kind = r % 3;
+    const int e = u - 5, t = e / 3, kind = e % 3;
     if (kind < 2) {
       const int i = 2 * t + kind;
-      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], sl2, -st.m_new[b]));
+      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i], sl2, -st.m_new));
       pin(x);
-      s[b][i] = x;
+      s[i] = x;
     } else {
-      const bf16x2 pp = bf16x2{(__bf16)s[b][2 * t], (__bf16)s[b][2 * t + 1]};
-      st.pp[b][t] = pp;
-      st.rs[b] += s[b][2 * t] + s[b][2 * t + 1];
-      pin(st.rs[b]);
+      const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
+      st.pp[t] = pp;
+      st.rs += s[2 * t] + s[2 * t + 1];
+      pin(st.rs);
       pin(pp);
     }
   }
@@ -483,7 +459,7 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16 (&s)[kNB], SoftmaxSta
 // (k-step (g-8)/4, d-block (g-8)%4).
 __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, const unsigned char* sk,
                                             const FragOffsets& fo) {
-  if (g < 8) return *reinterpret_cast<const bf16x8*>(sk + fo.krow + (((uint32_t)(2 * g) ^ fo.kx) << 4));
+  if (g < 8) return *reinterpret_cast<const bf16x8*>(sk + fo.k[g]);
   const int ks = (g - 8) >> 2, db = (g - 8) & 3;
   const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
   const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
@@ -505,39 +481,33 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
   for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
 #pragma unroll
   for (int slot = 0; slot < kSlots; ++slot) {
-    if ((slot & 1) == 0 && slot / 2 + kLookahead < 16)
-      fr[slot / 2 + kLookahead] = load_frag(slot / 2 + kLookahead, sv, sk, fo);
-    if ((slot & 7) == 1 && slot < 32) issue_load(ld, slot >> 3);
-    const int b = slot & 1;
-    if (slot < 16) {
-      const int d = slot >> 1;
-      mfma_qk(s_out[b], fr[d], qf[b][d], d == 0);
-    } else if (slot < 32) {
-      const int f = (slot >> 1) - 8;
-      o[f & 3][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[8 + f], pf[b][f >> 2], o[f & 3][b], 0, 0, 0);
+    if (slot + kLookahead < 16) fr[slot + kLookahead] = load_frag(slot + kLookahead, sv, sk, fo);
+    if ((slot & 7) == 1 && (slot >> 3) < 2 * kGroups) issue_load(ld, slot >> 3);
+    if (slot < 8) {
+      mfma_qk(s_out[0], fr[slot], qf[0][slot], slot == 0);
+    } else if (slot < 16) {
+      const int f = slot - 8;
+      o[f & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][f >> 2], o[f & 3][0], 0, 0, 0);
     } else {
-      lsum[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[b][(slot - 32) >> 1], lsum[b], 0, 0, 0);
+      lsum[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[0][slot - 16], lsum[0], 0, 0, 0);
     }
 #pragma unroll
     for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
-      softmax_unit(u, s_in, st, m_run, l_run, alpha, sl2);
+      softmax_unit(u, s_in[0], st, m_run[0], l_run[0], alpha[0], sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
+  l_run[0] += st.rs;
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
-    l_run[b] += st.rs[b];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-      pf[b][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[b][4 * ks], st.pp[b][4 * ks + 1], 0, 1, 2, 3),
-                                          __builtin_shufflevector(st.pp[b][4 * ks + 2], st.pp[b][4 * ks + 3], 0, 1, 2, 3),
-                                          0, 1, 2, 3, 4, 5, 6, 7);
-  }
+  for (int ks = 0; ks < 2; ++ks)
+    pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
+                                        __builtin_shufflevector(st.pp[4 * ks + 2], st.pp[4 * ks + 3], 0, 1, 2, 3),
+                                        0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
 // vmcnt_hi[15:14]) waiting until at most N of this wave's vector-memory
 // operations are outstanding.
-constexpr int kLoadsPerTile = 4;  // K and V loads of one tile per wave
+constexpr int kLoadsPerTile = 2 * kGroups;  // K and V loads of one tile per wave
 constexpr int kWaitVm(int n) { return 0x0F70 | n; }
 
 __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
@@ -628,18 +598,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     lane_off[i] = (uint32_t)(row * row_stride) + lane_chunk[i];
   }
   const uint32_t lds0 = lds_addr(smem);
-  const unsigned char* const sk0 = smem;
-  const unsigned char* const sv0 = smem + kBufs * kTileBytes;
   const uint32_t lk0 = lds0, lv0 = lds0 + kBufs * kTileBytes;
-  // Tile t's load (t past the last tile: the last tile again, into a buffer
-  // nobody reads, so that every iteration issues the same loads and the
-  // waits can count them).
-  auto load_of = [&](int t) {
+  // Tile t's load into buffer `buf` (= t % kBufs).  t past the last tile
+  // loads the last tile again, into a buffer nobody reads, so that every
+  // iteration issues the same loads and the waits can count them.
+  auto load_of = [&](int t, int buf) {
     const int tt = t < n_tiles ? t : n_tiles - 1;
     return prep_tile<kRPW>(tile_at(tw, tt), src, kvh, row_stride, wave, lane_off, lane_row, lane_chunk,
-                           lk0 + (t & (kBufs - 1)) * kTileBytes, lv0 + (t & (kBufs - 1)) * kTileBytes);
+                           lk0 + buf * kTileBytes, lv0 + buf * kTileBytes);
   };
-  if (n_tiles > 0) issue_tile(load_of(0));
+  if (n_tiles > 0) issue_tile(load_of(0, 0));
 
   // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
   // head-dim values of its query, for each of the 8 steps of 16 along D.
@@ -659,15 +627,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // The query fragments are only ever an MFMA operand: keep them in the
   // accumulation register file, leaving the VGPRs to the softmax.  (After
   // all loads are out, so that they overlap.)
-#pragma unroll
-  for (int b = 0; b < kNB; ++b)
-#pragma unroll
-    for (int ds = 0; ds < 8; ++ds) asm volatile("" : "+a"(qf[b][ds]));
   // Query fragments and tile 0 have landed (the builtin form lets the
   // compiler's own wait tracking see it); then tiles 1..kAhead-1 stream in.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
   if (n_tiles > 0)
-    for (int t = 1; t < kAhead; ++t) issue_tile(load_of(t));
+    for (int t = 1; t < kAhead; ++t) issue_tile(load_of(t, t));
 
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
@@ -691,23 +655,28 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   f32x16 sa[kNB], sb[kNB];
   const int q0 = q_begin + qb0;
 
+  // The first iteration's P V step reads the V buffer before tile 0's (its
+  // P is zero): fill that buffer with zeros so that the product is zero too.
+  // (No load writes it before the second pair's barrier.)
+  static_assert(kTileBytes == 64 * kWaves * 16, "one 16-byte store per thread");
+  *reinterpret_cast<u32x4*>(smem + (2 * kBufs - 1) * kTileBytes + 16 * tid) = u32x4{};
   __syncthreads();  // tile 0 is in LDS for everyone
-  if (n_tiles > 0) qk_tile(sk0, fo, qf, sa);
+  if (n_tiles > 0) qk_tile(smem, fo, qf, sa);
 
-  // Iteration j: mask S_j, then the region (S_{j+1}, softmax of S_j,
-  // P_{j-1} V_{j-1}, loads of tile j+kAhead), then O's rescale if the max
-  // moved.  Tile 0 has no predecessor: P is zero then, read against V_0's
-  // finite data.
+  // Iteration j (tile buffer B = j % kBufs): mask
+  // S_j, then the region (S_{j+1} from K buffer B+1, softmax of S_j, P_{j-1}
+  // V_{j-1} from V buffer B-1, loads of tile j+kAhead into buffer
+  // B+kAhead), then O's rescale if the max moved.  The last iteration
+  // computes scores of the tile after its own from the repeated last tile
+  // (finite data, unused).
   auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
+    const int B = j & (kBufs - 1);
     int lim[kNB];
     if (tile_limits(tile_at(tw, j), q0, wave_active, wave_lo, wave_hi, qrel_b, valid_b, lim))
       mask_tile(s_in, half, lim);
-    const TileLoad ld = load_of(j + kAhead);
-    // The last iteration recomputes scores of its own tile (unused).
-    const int kn = j + 1 < n_tiles ? j + 1 : j;
-    const int vp = j > 0 ? j - 1 : 0;
-    pipelined_region(sv0 + (vp & (kBufs - 1)) * kTileBytes, sk0 + (kn & (kBufs - 1)) * kTileBytes, fo, qf, pf, o,
-                     s_in, s_out, lsum, m_run, l_run, alpha, sl2, ld);
+    const TileLoad ld = load_of(j + kAhead, (B + kAhead) % kBufs);
+    pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
+                     pf, o, s_in, s_out, lsum, m_run, l_run, alpha, sl2, ld);
     rescale_o(o, lsum, alpha);
   };
 
@@ -725,7 +694,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0) pv_tile(sv0 + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, lsum);
+  if (n_tiles > 0) pv_tile(smem + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, lsum);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
