@@ -270,22 +270,12 @@ __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
   return f;
 }
 
-// One step of S^T = K Q^T written straight to VGPRs (the softmax reads the
-// scores with VALU instructions; the MFMA's own accumulator form would put
-// them in AGPRs and cost a copy per score).  The query fragment stays in
-// AGPRs.  The compiler does not see into the assembly, so readers of `acc`
-// are kept at least 19 wait states away by construction (every caller issues
-// 16 more MFMAs, or an explicit s_nop block, before the scores are read).
+// One step of S^T = K Q^T.  Every operand lives in VGPRs, and the compiler
+// sees the instruction, so it keeps the matrix-core hazards (result reads,
+// operand overwrites) itself.
 __device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& k, const bf16x8& q, bool first) {
-  if (first)
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "v"(q));
-  else
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "v"(q));
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, q, first ? f32x16{} : acc, 0, 0, 0);
 }
-
-// Wait states between the last score MFMA of the prologue and the first
-// VALU read of its result (a 32x32x16 MFMA needs at most 19).
-__device__ __forceinline__ void mfma_result_wait() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4"); }
 
 // S^T = K Q^T for one 32-key tile (the prologue's first tile).
 __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
@@ -296,25 +286,12 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
 #pragma unroll
     for (int b = 0; b < kNB; ++b) mfma_qk(s[b], kf, qf[b][ds], ds == 0);
   }
-  mfma_result_wait();
-}
-
-// The all-ones A operand: an MFMA of it against P^T adds every query's sum of
-// its bf16 probabilities (over the k-step's 16 keys) to all 32 rows of the
-// accumulator.  The matrix cores have slack and the vector ALUs do not.
-__device__ __forceinline__ bf16x8 ones_frag() {
-  return __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 }
 
 // O^T += V^T P^T for one 32-key tile (the last one); each V fragment serves
-// both query blocks.  lsum gets the tile's bf16 row sums.
+// both query blocks.
 __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
-                                        f32x16 (&o)[4][kNB], f32x16 (&lsum)[kNB]) {
-  const bf16x8 ones = ones_frag();
-#pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-    for (int b = 0; b < kNB; ++b) lsum[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[b][ks], lsum[b], 0, 0, 0);
+                                        f32x16 (&o)[4][kNB]) {
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
@@ -347,8 +324,8 @@ __device__ __forceinline__ void mask_tile(f32x16 (&s)[kNB], int half, const int 
 
 // Keys at tile offsets >= lim are past the range end (hi) or after the
 // lane's query (position q0 + qrel).  A tile past the wave's last query is
-// masked entirely.  Returns whether the tile needs masking at all.
-__device__ __forceinline__ bool tile_limits(const Tile& x, int q0, bool wave_active, int wave_lo, int wave_hi,
+// masked entirely.
+__device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_active, int wave_hi,
                                             const int (&qrel)[kNB], const bool (&valid)[kNB], int (&lim)[kNB]) {
   const bool live = wave_active && x.t0 <= wave_hi;
   const int a = q0 + 1 - x.t0;
@@ -359,32 +336,25 @@ __device__ __forceinline__ bool tile_limits(const Tile& x, int q0, bool wave_act
     e = e < 0 ? 0 : (e > kTileKeys ? kTileKeys : e);
     lim[b] = (live && valid[b]) ? e : 0;
   }
-  return !live || (x.t0 + kTileKeys > x.hi) || (x.t0 + kTileKeys - 1 > wave_lo);
 }
 
-// O and the bf16 row sums *= alpha (per query column), in place, for the
-// rare softmax that moved the running max.  Every register of the kernel is
+// O *= alpha (per query column), in place, for the rare softmax that moved
+// the running max (the wave-wide decision was taken with the max itself).  Every register of the kernel is
 // an ordinary VGPR (two waves per SIMD leave 256 per lane, enough for all of
 // them), so this is plain vector code.
 
-__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], f32x16 (&lsum)[kNB], const float (&alpha)[kNB]) {
-  bool any = false;
+__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alpha)[kNB], bool any_grow) {
+  if (any_grow) {
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) any |= alpha[b] != 1.f;
-  if (__any(any)) {
-#pragma unroll
-    for (int b = 0; b < kNB; ++b) {
+    for (int b = 0; b < kNB; ++b)
 #pragma unroll
       for (int db = 0; db < 4; ++db) o[db][b] *= alpha[b];
-      lsum[b] *= alpha[b];
-    }
   }
 }
 
-// One iteration's matrix and vector work as a fixed sequence of 18 MFMA
+// One iteration's matrix and vector work as a fixed sequence of 16 MFMA
 // slots: slots 0-7 compute S_{j+1} = K_{j+1} Q^T (K step d = slot), slots
-// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8), slots 16-17 add P_{j-1}'s
-// bf16 row sums (k-step slot - 16).  The softmax of S_j is cut into units of
+// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8).  The softmax of S_j is cut into units of
 // roughly equal VALU time and dealt out over the slots, so that every MFMA
 // has vector work to overlap with; LDS fragments are read three slots ahead,
 // and the two loads of tile j+5 (K rows, then V rows) go out at slots 1 and
@@ -393,13 +363,13 @@ __device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], f32x16 (&lsum)[kN
 // and scalar work issues while the other's matrix work runs.
 //
 // Units: 0-3 running max over four scores each (scores 4u..4u+3); 4 the
-// exchange with the other lane half and the new max (in exponent units),
-// and the start of the fp32 sum; 5-28 eight times (two exponentials, one
-// pack-and-fp32-sum) for score pairs; 29 the rescale factor and the sum's
-// rescale.
+// exchange with the other lane half, the new max (in exponent units) and
+// whether any lane of the wave moved it, and the start of the sums; 5-28
+// eight times (two exponentials, one pack-and-sum) for score pairs; 29 the
+// rescale factor and the sums' rescale.
 constexpr int kUnits = 30;
-constexpr int kSlots = 18;
-constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 8, 10, 12, 14, 15, 17, 19, 20, 22, 24, 26, 27, 29, 30};
+constexpr int kSlots = 16;
+constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 9, 11, 13, 15, 17, 19, 21, 23, 25, 27, 29, 30};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -411,14 +381,18 @@ __device__ __forceinline__ void pin(const T& x) {
 }
 
 struct SoftmaxState {
-  float mx;     // partial max of the tile's scores
-  float m_new;  // the max after this tile (lazily moved), exponent units
-  float rs;     // fp32 sum of this tile's probabilities
+  float mx;       // partial max of the tile's scores
+  float m_new;    // the max after this tile (lazily moved), exponent units
+  float rs;       // fp32 sum of this tile's probabilities
+  float rsb;      // sum of the bf16-rounded probabilities
+  bool any_grow;  // some lane of the wave moved its max (O needs rescaling)
   bf16x2 pp[8];
 };
 
+constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
+
 __device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float& m_run, float& l_run,
-                                             float& alpha, float sl2) {
+                                             float& lb_run, float& alpha, float sl2) {
   if (u < 4) {
     const int q = 4 * u;
     if (q == 0)
@@ -431,13 +405,17 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st,
     // max after the exchange.  The max moves only when it grows by more than
     // 2^8 in the exponent.
     const float mx = xmax32(st.mx) * sl2;
-    st.m_new = mx > m_run + kLazyRescaleLog2 ? mx : m_run;
+    const bool grow = mx > m_run + kLazyRescaleLog2;
+    st.m_new = grow ? mx : m_run;
+    st.any_grow = __any(grow);
     st.rs = -0.f;  // x + -0 is x: the first add folds away
+    st.rsb = -0.f;
     pin(st.m_new);
   } else if (u == kUnits - 1) {
     alpha = __builtin_amdgcn_exp2f(m_run - st.m_new);
     m_run = st.m_new;
     l_run *= alpha;
+    lb_run *= alpha;
   } else {
     const int e = u - 5, t = e / 3, kind = e % 3;
     if (kind < 2) {
@@ -449,7 +427,9 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st,
       const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
       st.pp[t] = pp;
       st.rs += s[2 * t] + s[2 * t + 1];
+      st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb, false);
       pin(st.rs);
+      pin(st.rsb);
       pin(pp);
     }
   }
@@ -471,11 +451,10 @@ __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, cons
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
                                                  const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
                                                  bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB],
-                                                 f32x16 (&s_out)[kNB], f32x16 (&lsum)[kNB], float (&m_run)[kNB],
-                                                 float (&l_run)[kNB], float (&alpha)[kNB], float sl2,
-                                                 const TileLoad& ld) {
+                                                 f32x16 (&s_out)[kNB], float (&m_run)[kNB], float (&l_run)[kNB],
+                                                 float (&lb_run)[kNB], float (&alpha)[kNB], float sl2,
+                                                 const TileLoad& ld, bool& any_grow) {
   SoftmaxState st;
-  const bf16x8 ones = ones_frag();
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
@@ -485,18 +464,18 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
     if ((slot & 7) == 1 && (slot >> 3) < 2 * kGroups) issue_load(ld, slot >> 3);
     if (slot < 8) {
       mfma_qk(s_out[0], fr[slot], qf[0][slot], slot == 0);
-    } else if (slot < 16) {
+    } else {
       const int f = slot - 8;
       o[f & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][f >> 2], o[f & 3][0], 0, 0, 0);
-    } else {
-      lsum[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[0][slot - 16], lsum[0], 0, 0, 0);
     }
 #pragma unroll
     for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
-      softmax_unit(u, s_in[0], st, m_run[0], l_run[0], alpha[0], sl2);
+      softmax_unit(u, s_in[0], st, m_run[0], l_run[0], lb_run[0], alpha[0], sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
+  any_grow = st.any_grow;
   l_run[0] += st.rs;
+  lb_run[0] += st.rsb;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
     pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
@@ -578,6 +557,26 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   const int n_tiles = tw.n;
 
+  // Within each range, the tiles from some index on need masking (they pass
+  // the range end, cross the diagonal or start after the wave's last query);
+  // the ones before are entirely visible to every query of the wave.  So a
+  // tile needs masking exactly when its index lies in [mA, firstB),
+  // [mB, firstC) or [mC, n).
+  auto first_masked = [&](int first, int n, int lo, int hi) {
+    if (!wave_active) return first;
+    int k = ((wave_hi - lo) >> 5) + 1;                    // starts after the last query
+    const int kd = ((wave_lo - lo - (kTileKeys - 1)) >> 5) + 1;  // crosses the diagonal
+    const int kp = (hi - lo) >> 5;                        // passes the range end
+    k = k < kd ? k : kd;
+    k = k < kp ? k : kp;
+    k = k < 0 ? 0 : (k > n ? n : k);
+    return first + k;
+  };
+  static_assert(kTileKeys == 32, "tile index = key offset >> 5");
+  const int mask_a = first_masked(0, tw.firstB, 0, tw.hiA);
+  const int mask_b = first_masked(tw.firstB, tw.firstC - tw.firstB, tw.loB, tw.hiB);
+  const int mask_c = first_masked(tw.firstC, tw.n - tw.firstC, tw.loC, tw.hiC);
+
   KvSource src;
   src.k_new = reinterpret_cast<const unsigned char*>(d.k_new);
   src.v_new = reinterpret_cast<const unsigned char*>(d.v_new);
@@ -636,18 +635,17 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
   f32x16 o[4][kNB];
-  f32x16 lsum[kNB];                            // sums of the bf16-rounded probabilities (every row alike)
-  float m_run[kNB], l_run[kNB];                // running max (exponent units); sum of the fp32 probabilities
-                                               // (lane's keys)
+  float m_run[kNB];                            // running max (exponent units)
+  float l_run[kNB], lb_run[kNB];               // sums of the fp32 / bf16-rounded probabilities (lane's keys)
   float alpha[kNB];                            // rescale factor of the last softmax
   bf16x8 pf[kNB][2];                           // P of the previous tile
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
-    lsum[b] = f32x16{};
     m_run[b] = kNoMax;
     l_run[b] = 0.f;
+    lb_run[b] = 0.f;
     alpha[b] = 1.f;
     pf[b][0] = pf[b][1] = bf16x8{};
   }
@@ -671,13 +669,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // (finite data, unused).
   auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
     const int B = j & (kBufs - 1);
-    int lim[kNB];
-    if (tile_limits(tile_at(tw, j), q0, wave_active, wave_lo, wave_hi, qrel_b, valid_b, lim))
+    if ((j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c) {
+      int lim[kNB];
+      tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
       mask_tile(s_in, half, lim);
+    }
+    bool any_grow;
     const TileLoad ld = load_of(j + kAhead, (B + kAhead) % kBufs);
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
-                     pf, o, s_in, s_out, lsum, m_run, l_run, alpha, sl2, ld);
-    rescale_o(o, lsum, alpha);
+                     pf, o, s_in, s_out, m_run, l_run, lb_run, alpha, sl2, ld, any_grow);
+    rescale_o(o, alpha, any_grow);
   };
 
   // Iterations go in pairs behind one barrier.  At a pair's start every tile
@@ -694,14 +695,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0) pv_tile(smem + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, lsum);
+  if (n_tiles > 0) pv_tile(smem + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
     const float lt = xsum32(l_run[b]);
-    const float ltb = lsum[b][0];  // the MFMA summed over both lane halves' keys
+    const float ltb = xsum32(lb_run[b]);
     const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
     const float inv = live ? 1.f / ltb : 0.f;
     if (valid_b[b]) {
