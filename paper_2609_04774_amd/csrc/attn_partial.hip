@@ -557,6 +557,23 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   const int n_tiles = tw.n;
 
+  // A work item that sees no key at all (a KV shard entirely after its
+  // queries) only writes its rows' empty result: O = 0, LSE = -inf.  The whole
+  // workgroup takes this exit together (n_tiles is the workgroup's).
+  if (n_tiles == 0) {
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) {
+      if (!valid_b[b]) continue;
+      const int64_t row = loff + qb0 + qrel_b[b];
+      float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
+#pragma unroll
+      for (int c = 0; c < kHeadDim / 8; ++c)
+        *reinterpret_cast<float4*>(orow + c * 8 + half * 4) = float4{0.f, 0.f, 0.f, 0.f};
+      if (half == 0) d.lse[row * Hq + head_b[b]] = -INFINITY;
+    }
+    return;
+  }
+
   // Within each range, the tiles from some index on need masking (they pass
   // the range end, cross the diagonal or start after the wave's last query);
   // the ones before are entirely visible to every query of the wave.  So a
