@@ -7,14 +7,17 @@
 //
 // How (FlashAttention-2 style online softmax, Dao 2023, with the running
 // max/sum recurrence of Milakov & Gimelshein 2018):
-//   * A workgroup of 4 wave64s (one per SIMD) owns 256 (query, head) rows that
-//     share one KV head: `heads_per_wg` query heads x `q_per_wg` consecutive
-//     positions.  Each wave owns two blocks of 32 rows, so every K or V
-//     fragment read from LDS feeds two MFMAs.
+//   * A workgroup of 8 wave64s (two per SIMD) owns 256 (query, head) rows
+//     that share one KV head: `heads_per_wg` query heads x `q_per_wg`
+//     consecutive positions.  Each wave owns one block of 32 rows.  Two waves
+//     per SIMD let one wave's vector and scalar work issue while the other's
+//     matrix work runs (a single wave issues one instruction at a time,
+//     whatever its type); the 256 registers per lane this leaves a wave hold
+//     all of its state in VGPRs.
 //   * Keys are visited in tiles of 32 along each key range (paged prefix,
 //     then the suffix ranges).  Tiles past the workgroup's last query are
 //     never visited; only tiles that cross the diagonal or a range end are
-//     masked.
+//     masked.  A work item that sees no key writes its empty result and exits.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane then holds one query's column, so the
 //     row max and row sum are in-lane plus one exchange with lane ^ 32, and
@@ -23,10 +26,8 @@
 //   * Software pipeline: iteration j runs S_{j+1} = K_{j+1} Q^T, the softmax
 //     of S_j and O += V_{j-1}^T P_{j-1} -- three independent streams -- as
 //     one fixed sequence of MFMA slots with the softmax dealt out between
-//     them, so the matrix cores and the VALU work side by side within each
-//     wave.  Iterations go in pairs that share one workgroup barrier and swap
-//     the two score register sets; each iteration loads tile j+5 into LDS
-//     with loads spread over its slots.
+//     them.  Iterations go in pairs that share one workgroup barrier and swap
+//     the two score register sets; each iteration loads tile j+5 into LDS.
 //   * LDS rows are 256 bytes; 16-byte chunks are XOR-swizzled by the row so
 //     that both the K reads (16 rows, one chunk) and the transposed V reads
 //     (4 rows, four chunks) hit distinct banks.
@@ -288,8 +289,7 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
   }
 }
 
-// O^T += V^T P^T for one 32-key tile (the last one); each V fragment serves
-// both query blocks.
+// O^T += V^T P^T for one 32-key tile (the last one).
 __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
                                         f32x16 (&o)[4][kNB]) {
 #pragma unroll
