@@ -338,20 +338,6 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
   }
 }
 
-// O *= alpha (per query column), in place, for the rare softmax that moved
-// the running max (the wave-wide decision was taken with the max itself).  Every register of the kernel is
-// an ordinary VGPR (two waves per SIMD leave 256 per lane, enough for all of
-// them), so this is plain vector code.
-
-__device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alpha)[kNB], bool any_grow) {
-  if (any_grow) {
-#pragma unroll
-    for (int b = 0; b < kNB; ++b)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) o[db][b] *= alpha[b];
-  }
-}
-
 // One iteration's matrix and vector work as a fixed sequence of 16 MFMA
 // slots: slots 0-7 compute S_{j+1} = K_{j+1} Q^T (K step d = slot), slots
 // 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8).  The softmax of S_j is cut into units of
@@ -365,11 +351,12 @@ __device__ __forceinline__ void rescale_o(f32x16 (&o)[4][kNB], const float (&alp
 // Units: 0-3 running max over four scores each (scores 4u..4u+3); 4 the
 // exchange with the other lane half, the new max (in exponent units) and
 // whether any lane of the wave moved it, and the start of the sums; 5-28
-// eight times (two exponentials, one pack-and-sum) for score pairs; 29 the
-// rescale factor and the sums' rescale.
-constexpr int kUnits = 30;
+// eight times (two exponentials, one pack-and-sum) for score pairs.  The
+// rescale of the sums and of O, needed only when the max moved, follows the
+// region (rescale).
+constexpr int kUnits = 29;
 constexpr int kSlots = 16;
-constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 9, 11, 13, 15, 17, 19, 21, 23, 25, 27, 29, 30};
+constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 9, 11, 12, 14, 16, 18, 20, 22, 23, 25, 27, 29};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -391,8 +378,7 @@ struct SoftmaxState {
 
 constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
-__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float& m_run, float& l_run,
-                                             float& lb_run, float& alpha, float sl2) {
+__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float m_run, float sl2) {
   if (u < 4) {
     const int q = 4 * u;
     if (q == 0)
@@ -411,11 +397,6 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st,
     st.rs = -0.f;  // x + -0 is x: the first add folds away
     st.rsb = -0.f;
     pin(st.m_new);
-  } else if (u == kUnits - 1) {
-    alpha = __builtin_amdgcn_exp2f(m_run - st.m_new);
-    m_run = st.m_new;
-    l_run *= alpha;
-    lb_run *= alpha;
   } else {
     const int e = u - 5, t = e / 3, kind = e % 3;
     if (kind < 2) {
@@ -452,8 +433,7 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
                                                  const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
                                                  bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB],
                                                  f32x16 (&s_out)[kNB], float (&m_run)[kNB], float (&l_run)[kNB],
-                                                 float (&lb_run)[kNB], float (&alpha)[kNB], float sl2,
-                                                 const TileLoad& ld, bool& any_grow) {
+                                                 float (&lb_run)[kNB], float sl2, const TileLoad& ld) {
   SoftmaxState st;
   bf16x8 fr[16];
 #pragma unroll
@@ -470,12 +450,23 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
     }
 #pragma unroll
     for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
-      softmax_unit(u, s_in[0], st, m_run[0], l_run[0], lb_run[0], alpha[0], sl2);
+      softmax_unit(u, s_in[0], st, m_run[0], sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
-  any_grow = st.any_grow;
-  l_run[0] += st.rs;
-  lb_run[0] += st.rsb;
+  // The tile's sums join the running ones; when some lane of the wave moved
+  // its max, the running sums and O are first rescaled by 2^(m_old - m_new)
+  // (exactly 1 in the lanes that did not move).
+  if (st.any_grow) {
+    const float alpha = __builtin_amdgcn_exp2f(m_run[0] - st.m_new);
+    l_run[0] = l_run[0] * alpha + st.rs;
+    lb_run[0] = lb_run[0] * alpha + st.rsb;
+#pragma unroll
+    for (int db = 0; db < 4; ++db) o[db][0] *= alpha;
+  } else {
+    l_run[0] += st.rs;
+    lb_run[0] += st.rsb;
+  }
+  m_run[0] = st.m_new;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
     pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
@@ -654,7 +645,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   f32x16 o[4][kNB];
   float m_run[kNB];                            // running max (exponent units)
   float l_run[kNB], lb_run[kNB];               // sums of the fp32 / bf16-rounded probabilities (lane's keys)
-  float alpha[kNB];                            // rescale factor of the last softmax
   bf16x8 pf[kNB][2];                           // P of the previous tile
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
@@ -663,7 +653,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     m_run[b] = kNoMax;
     l_run[b] = 0.f;
     lb_run[b] = 0.f;
-    alpha[b] = 1.f;
     pf[b][0] = pf[b][1] = bf16x8{};
   }
   // Scores of the current tile alternate between two register sets.
@@ -691,11 +680,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
       mask_tile(s_in, half, lim);
     }
-    bool any_grow;
     const TileLoad ld = load_of(j + kAhead, (B + kAhead) % kBufs);
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
-                     pf, o, s_in, s_out, m_run, l_run, lb_run, alpha, sl2, ld, any_grow);
-    rescale_o(o, alpha, any_grow);
+                     pf, o, s_in, s_out, m_run, l_run, lb_run, sl2, ld);
   };
 
   // Iterations go in pairs behind one barrier.  At a pair's start every tile
