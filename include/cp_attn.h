@@ -158,15 +158,21 @@ typedef struct cp_partial_desc {
 } cp_partial_desc;
 
 /*
- * Device workspace bytes cp_attn_partial needs for this descriptor set (the
- * device copy of the descriptors and the scheduled work list).  0 on invalid
- * arguments (and cp_last_error says why).
+ * Device workspace bytes cp_attn_partial needs for this descriptor set: the
+ * device copy of the descriptors and the scheduled work list, and, when the
+ * set has few work items with long key walks (a short suffix over a long
+ * cached prefix), one slot of 256 x (128 + 1) fp32 per piece the walks are
+ * split into (about a thousand pieces at most).  Deterministic in the
+ * descriptors and head counts.  0 on invalid arguments (and cp_last_error
+ * says why).
  */
 size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_descs,
                                       int32_t n_heads_q, int32_t n_heads_kv);
 
 /*
- * Partial attention of every descriptor, in one kernel launch.
+ * Partial attention of every descriptor, in one kernel launch (plus, when
+ * key walks were split, one launch that merges each walk's pieces exactly,
+ * by the log-sum-exp combination of paper Sec. 2.1).
  *   descs       host array of n_descs descriptors (read during the call only);
  *               n_descs == 0 is a no-op.  Descriptors may come from different
  *               requests (ragged lengths); output buffers must not overlap.

@@ -547,6 +547,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     tw.n = nA + nB + nC;
   }
   const int n_tiles = tw.n;
+  // This workgroup's share of the walk: all of it, or one piece.
+  const int t_first = it.t_end < 0 ? 0 : it.t_begin;
+  const int t_stop = it.t_end < 0 ? n_tiles : it.t_end;
 
   // A work item that sees no key at all (a KV shard entirely after its
   // queries) only writes its rows' empty result: O = 0, LSE = -inf.  The whole
@@ -614,7 +617,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     return prep_tile<kRPW>(tile_at(tw, tt), src, kvh, row_stride, wave, lane_off, lane_row, lane_chunk,
                            lk0 + buf * kTileBytes, lv0 + buf * kTileBytes);
   };
-  if (n_tiles > 0) issue_tile(load_of(0, 0));
+  if (n_tiles > 0) issue_tile(load_of(t_first, t_first & (kBufs - 1)));
 
   // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
   // head-dim values of its query, for each of the 8 steps of 16 along D.
@@ -634,11 +637,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // The query fragments are only ever an MFMA operand: keep them in the
   // accumulation register file, leaving the VGPRs to the softmax.  (After
   // all loads are out, so that they overlap.)
-  // Query fragments and tile 0 have landed (the builtin form lets the
-  // compiler's own wait tracking see it); then tiles 1..kAhead-1 stream in.
+  // Query fragments and the first tile have landed (the builtin form lets
+  // the compiler's own wait tracking see it); then the next kAhead-1 tiles
+  // stream in.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
   if (n_tiles > 0)
-    for (int t = 1; t < kAhead; ++t) issue_tile(load_of(t, t));
+    for (int t = t_first + 1; t < t_first + kAhead; ++t) issue_tile(load_of(t, t & (kBufs - 1)));
 
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
@@ -659,13 +663,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   f32x16 sa[kNB], sb[kNB];
   const int q0 = q_begin + qb0;
 
-  // The first iteration's P V step reads the V buffer before tile 0's (its
-  // P is zero): fill that buffer with zeros so that the product is zero too.
-  // (No load writes it before the second pair's barrier.)
+  // The first iteration's P V step reads the V buffer before the first
+  // tile's (its P is zero): fill that buffer with zeros so that the product
+  // is zero too.  (No load writes it before the second pair's barrier.)
   static_assert(kTileBytes == 64 * kWaves * 16, "one 16-byte store per thread");
-  *reinterpret_cast<u32x4*>(smem + (2 * kBufs - 1) * kTileBytes + 16 * tid) = u32x4{};
-  __syncthreads();  // tile 0 is in LDS for everyone
-  if (n_tiles > 0) qk_tile(smem, fo, qf, sa);
+  *reinterpret_cast<u32x4*>(smem + (kBufs + ((t_first + kBufs - 1) & (kBufs - 1))) * kTileBytes + 16 * tid) =
+      u32x4{};
+  __syncthreads();  // the first tile is in LDS for everyone
+  if (n_tiles > 0) qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
 
   // Iteration j (tile buffer B = j % kBufs): mask
   // S_j, then the region (S_{j+1} from K buffer B+1, softmax of S_j, P_{j-1}
@@ -690,16 +695,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // own); the two tiles issued after those may still be in flight.  After the
   // barrier every wave is also done with the iterations before the pair, the
   // last readers of the buffers its loads reuse (tile j+5 takes tile j-3's).
-  for (int j = 0; j < n_tiles; j += 2) {
+  for (int j = t_first; j < t_stop; j += 2) {
     __builtin_amdgcn_s_waitcnt(kWaitVm(2 * kLoadsPerTile));
     __syncthreads();
     iteration(j, sa, sb);
-    if (j + 1 >= n_tiles) break;
+    if (j + 1 >= t_stop) break;
     iteration(j + 1, sb, sa);
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0) pv_tile(smem + ((n_tiles - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
+  if (n_tiles > 0) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
@@ -709,7 +714,26 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     const float ltb = xsum32(lb_run[b]);
     const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
     const float inv = live ? 1.f / ltb : 0.f;
-    if (valid_b[b]) {
+    if (it.piece >= 0) {
+      // One piece of a split walk: its partial over its keys goes to the
+      // piece slot (row 32 * block + lane of the work item).
+      unsigned char* slot = p.pieces + (size_t)it.piece * kPieceBytes;
+      const int r = (kNB * wave + b) * 32 + l32;
+      float* orow = reinterpret_cast<float*>(slot) + (size_t)r * kHeadDim;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float4 v;
+          v.x = o[db][b][4 * q4 + 0] * inv;
+          v.y = o[db][b][4 * q4 + 1] * inv;
+          v.z = o[db][b][4 * q4 + 2] * inv;
+          v.w = o[db][b][4 * q4 + 3] * inv;
+          *reinterpret_cast<float4*>(orow + db * 32 + q4 * 8 + half * 4) = v;
+        }
+      if (half == 0)
+        reinterpret_cast<float*>(slot + kPieceOBytes)[r] = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
+    } else if (valid_b[b]) {
       const int64_t row = loff + qb0 + qrel_b[b];
       float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
 #pragma unroll
@@ -728,6 +752,64 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
 }
 
+// Exact combination of a split work item's pieces (disjoint key sets of the
+// same rows): LSE = M + ln sum_k e^{LSE_k - M}, O = sum_k e^{LSE_k - LSE} O_k,
+// a piece with LSE_k = -inf weighing 0 (and not read).  Each row of the item
+// is written to the descriptor's output where the unsplit item would have
+// written it.  32 lanes per row (float4 each), 8 rows per 256-thread block,
+// kRowsPerWG / 8 blocks per split item.
+constexpr int kMergeRowsPerBlock = 8;
+
+__global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restrict__ descs,
+                                                          const SplitItem* __restrict__ splits, PartialParams p) {
+  const int blocks_per_item = kRowsPerWG / kMergeRowsPerBlock;
+  const SplitItem sp = splits[blockIdx.x / blocks_per_item];
+  const int r = (blockIdx.x % blocks_per_item) * kMergeRowsPerBlock + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 31;
+  const DevDesc& d = descs[sp.desc];
+  // The row's place, as the attention kernel assigns it (block bi, lane l32).
+  const int bi = r >> 5, l32 = r & 31;
+  const int qblocks_per_head = p.q_per_wg >> 5;
+  const int kvh = sp.head_group / p.groups_per_kv;
+  const int head = kvh * (p.Hq / p.Hkv) + (sp.head_group % p.groups_per_kv) * p.heads_per_wg + bi / qblocks_per_head;
+  const int qrel = (bi % qblocks_per_head) * 32 + l32;
+  const int64_t qb0 = (int64_t)sp.q_block * p.q_per_wg;
+  const int64_t q_len = sp.chunk ? d.q_len[1] : d.q_len[0];
+  if (qb0 + qrel >= q_len) return;
+  const int64_t row = (sp.chunk ? d.local_off[1] : d.local_off[0]) + qb0 + qrel;
+
+  float m = -INFINITY;
+  for (int k = 0; k < sp.n_pieces; ++k) {
+    const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * kPieceBytes;
+    m = fmaxf(m, reinterpret_cast<const float*>(slot + kPieceOBytes)[r]);
+  }
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float lse = -INFINITY;
+  if (m != -INFINITY) {
+    float total = 0.f;
+    for (int k = 0; k < sp.n_pieces; ++k) {
+      const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * kPieceBytes;
+      const float lk = reinterpret_cast<const float*>(slot + kPieceOBytes)[r];
+      if (lk == -INFINITY) continue;
+      const float w = expf(lk - m);
+      total += w;
+      const float4 v = reinterpret_cast<const float4*>(slot)[(size_t)r * (kHeadDim / 4) + lane];
+      acc.x += w * v.x;
+      acc.y += w * v.y;
+      acc.z += w * v.z;
+      acc.w += w * v.w;
+    }
+    const float inv = 1.f / total;
+    acc.x *= inv;
+    acc.y *= inv;
+    acc.z *= inv;
+    acc.w *= inv;
+    lse = m + logf(total);
+  }
+  reinterpret_cast<float4*>(d.o + (row * p.Hq + head) * kHeadDim)[lane] = acc;
+  if (lane == 0) d.lse[row * p.Hq + head] = lse;
+}
+
 }  // namespace
 
 int launch_partial(const PartialParams& p, void* stream) {
@@ -736,6 +818,12 @@ int launch_partial(const PartialParams& p, void* stream) {
                      p.descs, p.items, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial launch: ") + hipGetErrorString(e));
+  if (p.n_splits > 0) {
+    const unsigned blocks = (unsigned)p.n_splits * (unsigned)(kRowsPerWG / kMergeRowsPerBlock);
+    hipLaunchKernelGGL(split_merge_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, p.descs, p.splits, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial merge launch: ") + hipGetErrorString(e));
+  }
   return CP_OK;
 }
 

@@ -8,6 +8,14 @@
 // interleaved so that item i lands on XCD i % 8 with all items of one KV head
 // group on the same XCD: the workgroups streaming one head's K/V share that
 // XCD's L2.
+//
+// Split key walks.  When a launch has few work items (a short suffix over a
+// long cached prefix: few query rows, many keys each), the GPU's 256 compute
+// units would mostly idle.  Then each item's walk of key tiles is cut into
+// pieces of at least kMinPieceTiles tiles, aiming at about kTargetPieces
+// pieces in all; each piece is its own workgroup and writes a partial result
+// (O, LSE over its keys) to the workspace, and split_merge combines an item's
+// pieces exactly (the same log-sum-exp combination as cp_attn_merge).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -139,8 +147,29 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
 struct Plan {
   std::vector<DevDesc> descs;
   std::vector<WorkItem> items;
+  std::vector<SplitItem> splits;
+  int64_t n_pieces = 0;
   Shape shape;
 };
+
+constexpr int64_t kSplitBelowItems = 512;  // split only launches with fewer non-empty items
+constexpr int64_t kTargetPieces = 1024;
+constexpr int64_t kMinPieceTiles = 32;     // 1024 keys: the prologue and merge stay small
+constexpr int64_t kMaxPieces = 64;
+
+// Key tiles of one work item's walk, exactly as the kernel counts them: the
+// paged prefix, then each suffix range clipped to the item's last query.
+int64_t item_tiles(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
+  constexpr int64_t T = 32;
+  const int64_t last = std::min(qb * q_per_wg + q_per_wg, d.q_len[chunk]) - 1;
+  const int64_t vis_end = d.q_begin[chunk] + last + 1;
+  int64_t n = (d.prefix_keys + T - 1) / T;
+  for (int s = 0; s < d.n_seg; ++s) {
+    const int64_t vis = std::min(d.seg_hi[s], vis_end);
+    if (vis > d.seg_lo[s]) n += (vis - d.seg_lo[s] + T - 1) / T;
+  }
+  return n;
+}
 
 int64_t item_keys(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
   const int64_t last = std::min(qb * q_per_wg + q_per_wg, d.q_len[chunk]) - 1;
@@ -167,20 +196,52 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
     int64_t cost;
     WorkItem w;
   };
-  std::vector<std::vector<Cand>> per_xcd(kXcds);
-  int64_t total = 0;
+  // Query blocks of every descriptor and chunk, with their tile counts.
+  struct Block {
+    int32_t desc, chunk, q_block;
+    int64_t keys, tiles;
+  };
+  std::vector<Block> blocks;
+  int64_t nonempty = 0, all_tiles = 0, max_tiles = 0;
   for (int i = 0; i < n_descs; ++i) {
     const DevDesc& d = out->descs[i];
     for (int c = 0; c < 2; ++c) {
       if (d.q_len[c] == 0) continue;
       const int64_t nqb = (d.q_len[c] + sh.q_per_wg - 1) / sh.q_per_wg;
       for (int64_t qb = 0; qb < nqb; ++qb) {
-        const int64_t keys = item_keys(d, c, qb, sh.q_per_wg);
-        for (int g = 0; g < n_groups; ++g) {
-          per_xcd[g % kXcds].push_back(Cand{keys, WorkItem{i, c, (int32_t)qb, g}});
-          ++total;
-        }
+        const int64_t tiles = item_tiles(d, c, qb, sh.q_per_wg);
+        blocks.push_back(Block{i, c, (int32_t)qb, item_keys(d, c, qb, sh.q_per_wg), tiles});
+        if (tiles > 0) nonempty += n_groups;
+        all_tiles += tiles * n_groups;
+        max_tiles = std::max(max_tiles, tiles);
       }
+    }
+  }
+  // Splitting pays when the longest walk is long against the piece size (the
+  // pieces' set-up and the merge pass are not free).
+  int64_t piece_tiles = 0;  // 0: no splitting in this launch
+  if (nonempty > 0 && nonempty < kSplitBelowItems && max_tiles >= 4 * kMinPieceTiles)
+    piece_tiles = std::max<int64_t>(kMinPieceTiles, (all_tiles + kTargetPieces - 1) / kTargetPieces);
+  out->splits.clear();
+  out->n_pieces = 0;
+  std::vector<std::vector<Cand>> per_xcd(kXcds);
+  int64_t total = 0;
+  for (const Block& b : blocks) {
+    const int64_t n_pieces = piece_tiles ? std::min<int64_t>(kMaxPieces, b.tiles / piece_tiles) : 1;
+    for (int g = 0; g < n_groups; ++g) {
+      if (n_pieces <= 1) {
+        per_xcd[g % kXcds].push_back(Cand{b.keys, WorkItem{b.desc, b.chunk, b.q_block, g, 0, -1, -1, 0}});
+        ++total;
+        continue;
+      }
+      out->splits.push_back(SplitItem{b.desc, b.chunk, b.q_block, g, (int32_t)out->n_pieces, (int32_t)n_pieces});
+      for (int64_t k = 0; k < n_pieces; ++k) {
+        const int32_t t0 = (int32_t)(b.tiles * k / n_pieces), t1 = (int32_t)(b.tiles * (k + 1) / n_pieces);
+        per_xcd[g % kXcds].push_back(
+            Cand{(t1 - t0) * 32, WorkItem{b.desc, b.chunk, b.q_block, g, t0, t1, (int32_t)(out->n_pieces + k), 0}});
+        ++total;
+      }
+      out->n_pieces += n_pieces;
     }
   }
   if (total > 0x7fffffffLL) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: work list beyond 2^31 workgroups");
@@ -204,8 +265,20 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   return CP_OK;
 }
 
-size_t items_offset(size_t n_descs) {
-  return (n_descs * sizeof(DevDesc) + kItemsAlign - 1) / kItemsAlign * kItemsAlign;
+size_t align_up(size_t x) { return (x + kItemsAlign - 1) / kItemsAlign * kItemsAlign; }
+
+// Workspace layout: descriptors | work items | split items | piece slots.
+struct Layout {
+  size_t items, splits, pieces, total;
+};
+
+Layout layout_of(const Plan& plan) {
+  Layout l;
+  l.items = align_up(plan.descs.size() * sizeof(DevDesc));
+  l.splits = align_up(l.items + plan.items.size() * sizeof(WorkItem));
+  l.pieces = align_up(l.splits + plan.splits.size() * sizeof(SplitItem));
+  l.total = l.pieces + (size_t)plan.n_pieces * kPieceBytes;
+  return l;
 }
 
 // Pinned host staging for the descriptor/work-list upload.  A slot is reused
@@ -268,7 +341,7 @@ extern "C" size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, i
   Plan plan;
   if (build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan) != CP_OK) return 0;
   clear_error();
-  return items_offset(plan.descs.size()) + plan.items.size() * sizeof(WorkItem);
+  return layout_of(plan).total;
 }
 
 extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
@@ -283,21 +356,24 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
     clear_error();
     return CP_OK;
   }
-  const size_t off = items_offset(plan.descs.size());
-  const size_t need = off + plan.items.size() * sizeof(WorkItem);
+  const Layout lay = layout_of(plan);
   if (!workspace) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace is NULL");
   if (!aligned(workspace, 256)) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace must be 256-byte aligned");
-  if (workspace_bytes < need)
-    return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(need) + " bytes");
-  std::vector<unsigned char> host(need, 0);
+  if (workspace_bytes < lay.total)
+    return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(lay.total) + " bytes");
+  // Only the tables are uploaded; the piece slots are written by the kernel.
+  std::vector<unsigned char> host(lay.pieces, 0);
   std::memcpy(host.data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
-  std::memcpy(host.data() + off, plan.items.data(), plan.items.size() * sizeof(WorkItem));
-  st = stage_and_copy(host.data(), need, workspace, (hipStream_t)stream);
+  std::memcpy(host.data() + lay.items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+  if (!plan.splits.empty())
+    std::memcpy(host.data() + lay.splits, plan.splits.data(), plan.splits.size() * sizeof(SplitItem));
+  st = stage_and_copy(host.data(), lay.pieces, workspace, (hipStream_t)stream);
   if (st != CP_OK) return st;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
   PartialParams p;
   p.descs = static_cast<const DevDesc*>(workspace);
-  p.items = reinterpret_cast<const WorkItem*>(static_cast<unsigned char*>(workspace) + off);
+  p.items = reinterpret_cast<const WorkItem*>(ws + lay.items);
   p.n_items = (int32_t)plan.items.size();
   p.Hq = n_heads_q;
   p.Hkv = n_heads_kv;
@@ -306,7 +382,10 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
   p.groups_per_kv = plan.shape.groups_per_kv;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.waves_per_wg = 4;
+  p.waves_per_wg = 8;
+  p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
+  p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
+  p.n_splits = (int32_t)plan.splits.size();
   st = launch_partial(p, stream);
   if (st == CP_OK) clear_error();
   return st;

@@ -52,13 +52,38 @@ struct DevDesc {
 };
 
 // One workgroup's unit: a block of query positions of one chunk of one
-// descriptor, for one group of query heads sharing a KV head.
+// descriptor, for one group of query heads sharing a KV head, over the key
+// tiles [t_begin, t_end) of its walk (t_end < 0: the whole walk).  A work item
+// whose walk is split over several workgroups ("pieces") writes each piece's
+// partial result to piece slot `piece` of the workspace; the pieces are then
+// merged into the descriptor's output (split_merge).  piece < 0: the item
+// writes its rows directly.
 struct WorkItem {
   int32_t desc;
   int32_t chunk;
   int32_t q_block;
   int32_t head_group;
+  int32_t t_begin;
+  int32_t t_end;
+  int32_t piece;
+  int32_t reserved;
 };
+
+// A work item that was split: its pieces occupy slots [first_piece,
+// first_piece + n_pieces).
+struct SplitItem {
+  int32_t desc;
+  int32_t chunk;
+  int32_t q_block;
+  int32_t head_group;
+  int32_t first_piece;
+  int32_t n_pieces;
+};
+
+// Workspace of one piece: fp32 O of the work item's 256 rows (row = 32 *
+// block + lane), then their LSE.
+constexpr size_t kPieceOBytes = (size_t)kRowsPerWG * kHeadDim * 4;
+constexpr size_t kPieceBytes = kPieceOBytes + (size_t)kRowsPerWG * 4;
 
 struct PartialParams {
   const DevDesc* descs;
@@ -71,7 +96,10 @@ struct PartialParams {
   int32_t groups_per_kv;  // (Hq / Hkv) / heads_per_wg
   float scale_log2;       // softmax scale * log2(e)
   float scale;            // softmax scale
-  int32_t waves_per_wg;   // 4 (two 32-row blocks per wave) or 8 (one block per wave)
+  int32_t waves_per_wg;   // 8 (one 32-row block per wave)
+  unsigned char* pieces;  // piece slots (kPieceBytes each), or null when nothing is split
+  const SplitItem* splits;
+  int32_t n_splits;
 };
 
 int launch_partial(const PartialParams& p, void* stream);

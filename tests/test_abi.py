@@ -195,6 +195,21 @@ def test_workspace_size_grows_with_work():
         cp.workspace_size([bad], 8, 2)
 
 
+def test_workspace_holds_piece_slots_for_split_walks():
+    """Few query rows over a long cached prefix: the launch has few work items,
+    so each item's key walk is split into pieces and the workspace grows by
+    one slot (fp32 O and LSE of 256 rows) per piece.  A launch with many items
+    is never split."""
+    piece = 256 * 128 * 4 + 256 * 4
+    # 64 rows, 4 of 32 query heads per workgroup -> 16 items of 2049-2050
+    # tiles; about 1024 pieces in all: pieces of 33 tiles, 62 per item.
+    split = cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8)
+    assert 16 * 62 * piece <= split < 16 * 62 * piece + (1 << 20)
+    # The 32K Llama-3-8B rank-0 shard: 4096 items, no pieces.
+    whole = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
+    assert whole < piece
+
+
 def _merge_status(n_parts=2, n_tokens=4, H=2, D=128, out=FAKE, lse_out=FAKE * 2, restore=None,
                   parts=None, out_bf16=0):
     o = (ctypes.c_void_p * max(1, n_parts))(*([FAKE * 3] * n_parts if parts is None else parts))

@@ -122,6 +122,25 @@ def test_pass_kv_and_prefix_only_partials(L, P, C, Hq, Hkv, seed):
             compare(f64(o), f64(lse), Or, Lr, f"rank {r} prefix only")
 
 
+# Launches with few work items, so the key walks are split into pieces of
+# >= 32 tiles whose partials are merged in the workspace: a long cached
+# prefix under a short suffix (the prefix-hit case), and a small-head shard
+# whose long second chunk spans two suffix ranges.
+@pytest.mark.parametrize("L,P,C,Hq,Hkv,seed", [(8392, 8192, 2, 8, 2, 61), (8192, 0, 8, 4, 4, 62),
+                                                (4200, 3072, 1, 16, 4, 63)])
+def test_split_key_walks_match_oracle(L, P, C, Hq, Hkv, seed):
+    prob = Problem(L, P, C, Hq, Hkv, seed)
+    for r in range(C):
+        o, lse, plan, rows = prob.gpu_rank(r)
+        Or, Lr = prob.oracle_rank(r)
+        compare(f64(o), f64(lse), Or, Lr, f"rank {r}")
+    # Pass-KV shards too: pieces of a walk over one shard's two chunks.
+    for s in range(min(C, 2)):
+        o, lse, _, _ = prob.gpu_rank(0, kv_rank=s, include_prefix=(s == 0))
+        Or, Lr = prob.oracle_rank(0, kv_rank=s, include_prefix=(s == 0))
+        compare(f64(o), f64(lse), Or, Lr, f"rank 0 shard {s}")
+
+
 def test_explicit_softmax_scale():
     prob = Problem(300, 0, 2, 8, 2, 31)
     o, lse, _, _ = prob.gpu_rank(0, scale=0.05)
