@@ -28,9 +28,12 @@
 //     one fixed sequence of MFMA slots with the softmax dealt out between
 //     them.  Iterations go in pairs that share one workgroup barrier and swap
 //     the two score register sets; each iteration loads tile j+5 into LDS.
-//   * LDS rows are 256 bytes; 16-byte chunks are XOR-swizzled by the row so
-//     that both the K reads (16 rows, one chunk) and the transposed V reads
-//     (4 rows, four chunks) hit distinct banks.
+//   * LDS tiles are stored by 16-key halves and 16-byte columns: column c of
+//     a half holds head-dim chunk c (8 values) of its 16 keys, key k at slot
+//     k ^ 4(c % 4).  The K reads (16 keys, one column) and the transposed V
+//     reads (4 keys, four columns) then hit every bank once, and each lane's
+//     fragment addresses differ only by constants, so one tile's 16 fragment
+//     reads need four address registers.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -50,20 +53,22 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;                    // wave64s per workgroup, two per SIMD
 constexpr int kNB = 1;                       // blocks of 32 rows per wave
-constexpr int kGroups = 32 / kWaves / 4;     // 4-row groups of each tile one wave loads
 constexpr int kTileKeys = 32;
 constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
 constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
 constexpr int kRowBytes = kHeadDim * 2;
 constexpr int kTileBytes = kTileKeys * kRowBytes;
 
-// 16-byte chunk swizzle of a 256-byte LDS row (64 banks x 4 bytes on gfx950):
-// rows 0..15 get 16 distinct XOR masks, and any 4 rows r0..r0+3 (r0 % 4 == 0)
-// differ in mask bits 2-3 -- so the 16-row K reads and the 4-row x 4-chunk
-// transposed V reads each touch every bank once.
-__device__ __forceinline__ int swz(int key) { return ((key & 3) << 2) | ((key >> 2) & 3); }
-__device__ __forceinline__ int lds_off(int key, int chunk) {
-  return key * kRowBytes + ((chunk ^ swz(key)) << 4);
+// LDS byte offset of head-dim chunk c (16 bytes) of tile key `key` within a
+// tile buffer (64 banks x 4 bytes on gfx950).  A half (16 keys) is 16
+// columns of 256 bytes; in column c, key k sits at slot k ^ 4(c % 4).  Any 16
+// keys of one column fill 256 bytes (every bank once), and keys k0..k0+3
+// (k0 % 4 == 0) of four columns c0..c0+3 (c0 % 4 == 0) occupy 16 distinct
+// slots.
+constexpr int kHalfBytes = 16 * kRowBytes;
+constexpr int kColBytes = 16 * 16;
+__device__ __forceinline__ int lds_off(int key, int c) {
+  return (key >> 4) * kHalfBytes + c * kColBytes + (((key & 15) ^ (4 * (c & 3))) << 4);
 }
 
 __device__ __forceinline__ s16x4 ds_read_tr16(const unsigned char* p) {
@@ -93,6 +98,10 @@ struct Tile {
   bool paged;
 };
 
+// A select of two values (never of two variables' addresses, which would
+// put both variables in scratch memory).
+__device__ __forceinline__ int sel(bool c, int a, int b) { return c ? a : b; }
+
 __device__ __forceinline__ Tile tile_at(const TileWalk w, int t) {
   const bool gB = t >= w.firstB, gC = t >= w.firstC;
   Tile x;
@@ -121,13 +130,18 @@ struct KvSource {
 // byte m0 + 16*l.  Issued as inline assembly so the compiler does not treat
 // every later LDS read as depending on it (it cannot tell the two buffers
 // apart); the kernel waits for these loads itself (vmcnt) before the barrier
-// that publishes a tile.
+// that publishes a tile.  The base and the LDS address are wave-uniform; the
+// lane reads place them in scalar registers however the compiler carried
+// them.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  const uint64_t b = (uint64_t)(uintptr_t)sbase;
+  const uint64_t bs = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\t" ::"s"(lds_base),
-      "v"(voff), "s"(sbase)
+      "global_load_lds_dwordx4 %1, %2\n\t" ::"s"(__builtin_amdgcn_readfirstlane((int)lds_base)),
+      "v"(voff), "s"((const void*)(uintptr_t)bs)
       : "memory", "m0");
 }
 
@@ -136,42 +150,40 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
 }
 
 // This wave's share of one K/V tile load, prepared ahead of the slots that
-// issue it.  Wave w fills tile rows RPW*w .. RPW*w + RPW-1; lane l of load i
-// carries row RPW*w + 4i + l/16, physical chunk l%16, i.e. logical chunk
-// (l%16) ^ swz(row).  The address is a wave-uniform base (tile start, KV
-// head) plus a per-lane offset `lane_off[i]` = row_in_tile * row_stride + 16 *
-// logical chunk.  In the last tile of a suffix range, rows past the visible
-// end read the last visible row instead (in range; those keys are masked).
+// issue it: 1 KB of K and 1 KB of V, i.e. four LDS columns (4g .. 4g+3, g =
+// wave % 4) of tile half wave / 4.  Lane l fills slot l % 16 of column
+// 4g + l/16, so it carries that column's chunk of half key (l % 16) ^ 4(l/16)
+// (see lds_off).  The address is a wave-uniform base (tile start, KV head)
+// plus a per-lane offset `lane_off` = row_in_tile * row_stride + 16 * column.
+// In the last tile of a suffix range, rows past the visible end read the
+// last visible row instead (in range; those keys are masked).
+static_assert(kWaves * 4 * kColBytes == kTileBytes, "eight waves, 1 KB of the tile each");
 struct TileLoad {
   const unsigned char* kb;
   const unsigned char* vb;
-  uint32_t off[kGroups];
-  uint32_t lk[kGroups], lv[kGroups];  // LDS destinations of the row groups
+  uint32_t off;
+  uint32_t lk, lv;  // LDS destinations
 };
 
-template <int RPW>
 __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src, int kvh, int row_stride, int wave,
-                                              const uint32_t (&lane_off)[RPW / 4], const int (&lane_row)[RPW / 4],
-                                              const uint32_t (&lane_chunk)[RPW / 4], uint32_t sk, uint32_t sv) {
-  static_assert(RPW == 4 * kGroups, "row groups of four per wave");
-  const int row0 = wave * RPW;
+                                              uint32_t lane_off, int lane_row, uint32_t lane_col, uint32_t sk,
+                                              uint32_t sv) {
+  const int row0 = (wave >> 2) * 16;  // first tile row of this wave's half
+  const uint32_t dst = (uint32_t)((wave >> 2) * kHalfBytes + (wave & 3) * 4 * kColBytes);
   TileLoad t;
-#pragma unroll
-  for (int i = 0; i < kGroups; ++i) {
-    t.off[i] = lane_off[i];
-    t.lk[i] = sk + (uint32_t)((row0 + 4 * i) * kRowBytes);
-    t.lv[i] = sv + (uint32_t)((row0 + 4 * i) * kRowBytes);
-  }
+  t.off = lane_off;
+  t.lk = sk + dst;
+  t.lv = sv + dst;
   if (x.paged) {
-    // Prefix tiles start at multiples of 32 keys, so this wave's rows lie in
+    // Prefix tiles start at multiples of 32 keys, so this wave's half is
     // logical cache block t0/16 + row0/16 (clamped to the last block); the
-    // lane offsets use the row within the tile, so step back by the block's
+    // lane offsets use the row within the tile, so step back by the half's
     // first tile row.  Wave-uniform index: a scalar load.
     int lb = (x.t0 >> 4) + (row0 >> 4);
     const int last = ((x.vis + kBlockTokens - 1) >> 4) - 1;
     lb = lb < last ? lb : last;
     const int64_t blk = ((const __attribute__((address_space(4))) int32_t*)src.block_table)[lb];
-    const int64_t base = (blk * kBlockTokens - (row0 & ~(kBlockTokens - 1))) * row_stride + kvh * (kHeadDim * 2);
+    const int64_t base = (blk * kBlockTokens - row0) * row_stride + kvh * (kHeadDim * 2);
     t.kb = src.k_cache + base;
     t.vb = src.v_cache + base;
   } else {
@@ -180,28 +192,24 @@ __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src
     t.vb = src.v_new + base;
     if (x.t0 + kTileKeys > x.vis) {
       const int clamp_row = x.vis - 1 - x.t0;
-#pragma unroll
-      for (int i = 0; i < kGroups; ++i) {
-        const int r = lane_row[i] < clamp_row ? lane_row[i] : clamp_row;
-        t.off[i] = __umul24((uint32_t)r, (uint32_t)row_stride) + lane_chunk[i];
-      }
+      const int r = lane_row < clamp_row ? lane_row : clamp_row;
+      t.off = __umul24((uint32_t)r, (uint32_t)row_stride) + lane_col;
     }
   }
   return t;
 }
 
-// Load q (0 .. 2*kGroups-1) of a prepared tile: K or V rows of group q/2.
+// Load q (0: K, 1: V) of a prepared tile.
 __device__ __forceinline__ void issue_load(const TileLoad& t, int q) {
-  const int i = q >> 1;
   if (q & 1)
-    dma16(t.vb, t.off[i], t.lv[i]);
+    dma16(t.vb, t.off, t.lv);
   else
-    dma16(t.kb, t.off[i], t.lk[i]);
+    dma16(t.kb, t.off, t.lk);
 }
 
 __device__ __forceinline__ void issue_tile(const TileLoad& t) {
-#pragma unroll
-  for (int q = 0; q < 2 * kGroups; ++q) issue_load(t, q);
+  issue_load(t, 0);
+  issue_load(t, 1);
 }
 
 // max(a, b, c) in one v_maximum3_f32 (NaN-propagating maximum).  fmaxf on
@@ -239,36 +247,44 @@ constexpr float kNoMax = -1e30f;
 constexpr float kLn2 = 0.69314718055994531f;
 
 // Per-lane LDS byte offsets of the fragments in buffer 0 (buffer b adds
-// b * kTileBytes: one scalar-plus-vector add per fragment and tile).
-//   K (A operand of S^T = K Q^T): for step ds the lane reads tile row l32,
-//   logical chunk 2ds+half: k[ds] = l32 * 256 + ((2ds) ^ swz(l32) ^ half) * 16.
+// b * kTileBytes: one scalar-plus-vector add per offset and tile; the rest
+// are instruction immediates).
+//   K (A operand of S^T = K Q^T): for step ds the lane reads tile key l32,
+//   chunk c = 2ds + half.  c % 4 = 2(ds % 2) + half, so
+//   K(ds) = k[ds % 2] + (ds / 2) * 1024.
 //   V (A operand of O^T += V^T P^T, transposed 64-bit reads): for k-step ks
-//   and head-dim block db the group's 16 lanes read rows
-//   kbase + i/4 (kbase = 16ks + 4half, +8 for the second half of the slots) at
-//   columns d0 + 4(i%4), d0 = 32db + 16(group&1).  swz of those rows does not
-//   depend on ks, so ks is a constant +4096 and 4 db x 2 halves need offsets
-//   (these include the start of the V buffers, kBufs * kTileBytes).
+//   and head-dim block db the group's 16 lanes read keys
+//   16ks + 8r + 4half + i/4 (r = 0, 1: the two 8-byte halves of the
+//   fragment) at head-dim 32db + 16(group&1) + 4(i%4), i.e. chunk
+//   c = 4db + cc, cc = 2(group&1) + (i%4)/2, byte 8(i%2) of it.  c % 4 = cc
+//   for every db, so V(db, ks, r) = v[r] + db * 1024 + ks * 4096 (v includes
+//   the start of the V buffers, kBufs * kTileBytes).
 struct FragOffsets {
-  uint32_t k[8];
-  uint32_t v[4][2];
+  uint32_t k[2];
+  uint32_t v[2];
 };
 
 __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
   FragOffsets f;
   const int l32 = lane & 31, half = lane >> 5, grp = lane >> 4, gi = lane & 15;
 #pragma unroll
-  for (int ds = 0; ds < 8; ++ds) f.k[ds] = (uint32_t)(l32 * kRowBytes + (((2 * ds) ^ swz(l32) ^ half) << 4));
-  const int row1 = half * 4 + (gi >> 2);
-  const int row2 = row1 + 8;
+  for (int e = 0; e < 2; ++e) f.k[e] = (uint32_t)lds_off(l32, 2 * e + half);
+  const int cc = 2 * (grp & 1) + ((gi & 3) >> 1);
 #pragma unroll
-  for (int db = 0; db < 4; ++db) {
-    const int dcol = db * 32 + (grp & 1) * 16 + 4 * (gi & 3);
-    const int c = dcol >> 3;
-    const int e = (dcol & 7) * 2;
-    f.v[db][0] = (uint32_t)(kBufs * kTileBytes + row1 * kRowBytes + ((c ^ swz(row1)) << 4) + e);
-    f.v[db][1] = (uint32_t)(kBufs * kTileBytes + row2 * kRowBytes + ((c ^ swz(row2)) << 4) + e);
-  }
+  for (int r = 0; r < 2; ++r)
+    f.v[r] = (uint32_t)(kBufs * kTileBytes + lds_off(8 * r + 4 * half + (gi >> 2), cc) + 8 * (gi & 1));
   return f;
+}
+
+__device__ __forceinline__ const unsigned char* k_frag_addr(const unsigned char* sk, const FragOffsets& fo, int ds) {
+  return sk + fo.k[ds & 1] + (ds >> 1) * 4 * kColBytes;
+}
+
+__device__ __forceinline__ bf16x8 v_frag(const unsigned char* sv, const FragOffsets& fo, int ks, int db) {
+  const int c = db * 4 * kColBytes + ks * kHalfBytes;
+  const s16x4 lo4 = ds_read_tr16(sv + fo.v[0] + c);
+  const s16x4 hi4 = ds_read_tr16(sv + fo.v[1] + c);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // One step of S^T = K Q^T.  Every operand lives in VGPRs, and the compiler
@@ -283,7 +299,7 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
                                         f32x16 (&s)[kNB]) {
 #pragma unroll
   for (int ds = 0; ds < 8; ++ds) {
-    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + fo.k[ds]);
+    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, ds));
 #pragma unroll
     for (int b = 0; b < kNB; ++b) mfma_qk(s[b], kf, qf[b][ds], ds == 0);
   }
@@ -296,9 +312,7 @@ __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffse
   for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
-      const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
-      const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+      const bf16x8 vf = v_frag(sv, fo, ks, db);
 #pragma unroll
       for (int b = 0; b < kNB; ++b) o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
     }
@@ -420,11 +434,8 @@ __device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st,
 // (k-step (g-8)/4, d-block (g-8)%4).
 __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, const unsigned char* sk,
                                             const FragOffsets& fo) {
-  if (g < 8) return *reinterpret_cast<const bf16x8*>(sk + fo.k[g]);
-  const int ks = (g - 8) >> 2, db = (g - 8) & 3;
-  const s16x4 lo4 = ds_read_tr16(sv + fo.v[db][0] + ks * 16 * kRowBytes);
-  const s16x4 hi4 = ds_read_tr16(sv + fo.v[db][1] + ks * 16 * kRowBytes);
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+  if (g < 8) return *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, g));
+  return v_frag(sv, fo, (g - 8) >> 2, (g - 8) & 3);
 }
 
 // s_in: S_j (masked), turned into P_j; s_out: receives S_{j+1}.  pf: P_{j-1}
@@ -441,7 +452,7 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
 #pragma unroll
   for (int slot = 0; slot < kSlots; ++slot) {
     if (slot + kLookahead < 16) fr[slot + kLookahead] = load_frag(slot + kLookahead, sv, sk, fo);
-    if ((slot & 7) == 1 && (slot >> 3) < 2 * kGroups) issue_load(ld, slot >> 3);
+    if ((slot & 7) == 1) issue_load(ld, slot >> 3);
     if (slot < 8) {
       mfma_qk(s_out[0], fr[slot], qf[0][slot], slot == 0);
     } else {
@@ -477,13 +488,12 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
 // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
 // vmcnt_hi[15:14]) waiting until at most N of this wave's vector-memory
 // operations are outstanding.
-constexpr int kLoadsPerTile = 2 * kGroups;  // K and V loads of one tile per wave
+constexpr int kLoadsPerTile = 2;  // K and V loads of one tile per wave
 constexpr int kWaitVm(int n) { return 0x0F70 | n; }
 
 __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
                                                                      const WorkItem* __restrict__ items,
                                                                      PartialParams p) {
-  constexpr int kRPW = kTileKeys / kWaves;  // tile rows each wave loads
   // LDS: kBufs K tile buffers, then kBufs V tile buffers; tile t uses buffer
   // t % kBufs of each.
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kBufs * kTileBytes];
@@ -596,17 +606,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   src.block_table = d.block_table;
   src.P = (int)d.P;
 
-  // Per-lane part of the tile load addresses (see prep_tile).
+  // Per-lane part of the tile load addresses (see prep_tile): column
+  // 4(wave % 4) + lane / 16 of half wave / 4, slot lane % 16.
   const int row_stride = Hkv * kHeadDim * 2;
-  uint32_t lane_off[kRPW / 4], lane_chunk[kRPW / 4];
-  int lane_row[kRPW / 4];
-#pragma unroll
-  for (int i = 0; i < kRPW / 4; ++i) {
-    const int row = wave * kRPW + 4 * i + (lane >> 4);
-    lane_row[i] = row;
-    lane_chunk[i] = (uint32_t)(((lane & 15) ^ swz(row)) << 4);
-    lane_off[i] = (uint32_t)(row * row_stride) + lane_chunk[i];
-  }
+  const int lane_row = (wave >> 2) * 16 + ((lane & 15) ^ (4 * (lane >> 4)));
+  const uint32_t lane_col = (uint32_t)((4 * (wave & 3) + (lane >> 4)) * 16);
+  const uint32_t lane_off = (uint32_t)(lane_row * row_stride) + lane_col;
   const uint32_t lds0 = lds_addr(smem);
   const uint32_t lk0 = lds0, lv0 = lds0 + kBufs * kTileBytes;
   // Tile t's load into buffer `buf` (= t % kBufs).  t past the last tile
@@ -614,8 +619,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // iteration issues the same loads and the waits can count them.
   auto load_of = [&](int t, int buf) {
     const int tt = t < n_tiles ? t : n_tiles - 1;
-    return prep_tile<kRPW>(tile_at(tw, tt), src, kvh, row_stride, wave, lane_off, lane_row, lane_chunk,
-                           lk0 + buf * kTileBytes, lv0 + buf * kTileBytes);
+    return prep_tile(tile_at(tw, tt), src, kvh, row_stride, wave, lane_off, lane_row, lane_col,
+                     lk0 + buf * kTileBytes, lv0 + buf * kTileBytes);
   };
   if (n_tiles > 0) issue_tile(load_of(t_first, t_first & (kBufs - 1)));
 
@@ -634,15 +639,37 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       qf[b][ds] = valid_b[b] ? v : bf16x8{};
     }
   }
-  // The query fragments are only ever an MFMA operand: keep them in the
-  // accumulation register file, leaving the VGPRs to the softmax.  (After
-  // all loads are out, so that they overlap.)
   // Query fragments and the first tile have landed (the builtin form lets
   // the compiler's own wait tracking see it); then the next kAhead-1 tiles
   // stream in.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0)
-    for (int t = t_first + 1; t < t_first + kAhead; ++t) issue_tile(load_of(t, t & (kBufs - 1)));
+
+  // Load cursor.  Within a suffix range a tile's rows are the previous
+  // tile's plus 32, so the common tile load only advances two pointers.
+  // The full computation is left to the tiles of the paged prefix (a block
+  // lookup each), the first and the (possibly clamped) last tile of each
+  // suffix range, and the repeats past the last tile; `cur_full` is the
+  // next such tile.
+  const int64_t tile_step = (int64_t)kTileKeys * row_stride;
+  auto next_full = [fB = tw.firstB, fC = tw.firstC, n = n_tiles](int t) {
+    if (t + 1 < fB) return t + 1;
+    int f = n;
+    f = sel(fB > t && fB < f, fB, f);
+    f = sel(fC - 1 > t && fC - 1 < f, fC - 1, f);
+    f = sel(fC > t && fC < f, fC, f);
+    f = sel(n - 1 > t && n - 1 < f, n - 1, f);
+    return sel(f > t, f, t + 1);
+  };
+  TileLoad cur = {};
+  int cur_full = 0;
+  if (n_tiles > 0) {
+    for (int t = t_first + 1; t < t_first + kAhead; ++t) {
+      cur = load_of(t, t & (kBufs - 1));
+      issue_tile(cur);
+    }
+    cur_full = next_full(t_first + kAhead - 1);
+  }
+  const uint32_t wave_dst = (uint32_t)((wave >> 2) * kHalfBytes + (wave & 3) * 4 * kColBytes);
 
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
@@ -685,7 +712,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
       mask_tile(s_in, half, lim);
     }
-    const TileLoad ld = load_of(j + kAhead, (B + kAhead) % kBufs);
+    const int t = j + kAhead, buf = (B + kAhead) % kBufs;
+    TileLoad ld;
+    if (t >= cur_full) {
+      ld = load_of(t, buf);
+      cur_full = next_full(t);
+    } else {
+      ld.kb = cur.kb + tile_step;
+      ld.vb = cur.vb + tile_step;
+      ld.off = lane_off;
+      ld.lk = lk0 + buf * kTileBytes + wave_dst;
+      ld.lv = lv0 + buf * kTileBytes + wave_dst;
+    }
+    cur = ld;
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
                      pf, o, s_in, s_out, m_run, l_run, lb_run, sl2, ld);
   };
