@@ -22,7 +22,7 @@
 //     v_mfma_f32_32x32x16_bf16: a lane then holds one query's column, so the
 //     row max and row sum are in-lane plus one exchange with lane ^ 32, and
 //     the probabilities feed O^T += V^T P^T directly from registers.  V^T
-//     fragments come from the row-major V tile through ds_read_b64_tr_b16.
+//     fragments come from the key-major V tile through ds_read_b64_tr_b16.
 //   * Software pipeline: iteration j runs S_{j+1} = K_{j+1} Q^T, the softmax
 //     of S_j and O += V_{j-1}^T P_{j-1} -- three independent streams -- as
 //     one fixed sequence of MFMA slots with the softmax dealt out between
@@ -32,8 +32,8 @@
 //     a half holds head-dim chunk c (8 values) of its 16 keys, key k at slot
 //     k ^ 4(c % 4).  The K reads (16 keys, one column) and the transposed V
 //     reads (4 keys, four columns) then hit every bank once, and each lane's
-//     fragment addresses differ only by constants, so one tile's 16 fragment
-//     reads need four address registers.
+//     fragment addresses differ only by constants, so the 24 LDS reads of one
+//     tile's 16 fragments need four address registers.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
