@@ -7,9 +7,9 @@
 // Optionally each rank-local row is written to its place in the original
 // sequence order (the restore step of paper Sec. 2.1).
 //
-// Layout: one (token, head) row of 128 fp32 is read by 32 lanes as float4,
-// so a wave64 merges two rows and a 256-thread block eight; every partial's
-// row is one fully coalesced 512-byte read.
+// Layout: one (token, head) row of 128 fp32 is read by 32 lanes as float4
+// (every partial's row is one fully coalesced 512-byte read); each 32-lane
+// group merges two rows, a 256-thread block sixteen.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -20,7 +20,10 @@ namespace cpattn {
 
 namespace {
 
-constexpr int kRowsPerBlock = 8;
+constexpr int kRowsPerGroup = 2;                      // rows merged by one 32-lane group
+constexpr int kRowsPerBlock = 8 * kRowsPerGroup;       // 256 threads = 8 groups
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
   // Round-to-nearest-even conversion; gfx950 emits v_cvt_pk_bf16_f32.
@@ -28,61 +31,87 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
   return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
 }
 
+// Each 32-lane group merges two rows: first every partial's LSE of both rows
+// (so their latencies overlap), then the partial O rows that carry weight,
+// all in flight together.  O is read and written with non-temporal hints:
+// every byte is touched once, and streaming it past the caches measured
+// about 20% faster than plain loads and stores on the 4-partial merge of the
+// 32K shard.
 __global__ __launch_bounds__(256) void lse_merge_kernel(MergeParams p) {
-  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 5);
   const int lane = threadIdx.x & 31;
   const int64_t n_rows = p.n_tokens * p.n_heads;
-  if (row >= n_rows) return;
-  const int64_t tok = row / p.n_heads;
-  const int head = (int)(row - tok * p.n_heads);
+  const int64_t row0 = (int64_t)blockIdx.x * kRowsPerBlock + kRowsPerGroup * (threadIdx.x >> 5);
+  if (row0 >= n_rows) return;
 
-  float l[CP_MAX_MERGE_PARTS];
-  float m = -INFINITY;
+  float l[kRowsPerGroup][CP_MAX_MERGE_PARTS];
 #pragma unroll
   for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i) {
     if (i < p.n_parts) {
-      l[i] = p.lse[i][row];
-      m = fmaxf(m, l[i]);
+#pragma unroll
+      for (int r = 0; r < kRowsPerGroup; ++r) l[r][i] = row0 + r < n_rows ? p.lse[i][row0 + r] : -INFINITY;
     }
   }
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float lse_out = -INFINITY;
-  if (m != -INFINITY) {
-    float w[CP_MAX_MERGE_PARTS];
+  // Weights c = e^{LSE_i - M} / sum_k e^{LSE_k - M} (0 for a -inf partial and
+  // for rows where every partial is -inf).
+  float c[kRowsPerGroup][CP_MAX_MERGE_PARTS];
+  float lse_out[kRowsPerGroup];
+#pragma unroll
+  for (int r = 0; r < kRowsPerGroup; ++r) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i)
+      if (i < p.n_parts) m = fmaxf(m, l[r][i]);
     float total = 0.f;
 #pragma unroll
     for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i) {
       if (i < p.n_parts) {
-        w[i] = (l[i] == -INFINITY) ? 0.f : expf(l[i] - m);
-        total += w[i];
+        c[r][i] = (m == -INFINITY || l[r][i] == -INFINITY) ? 0.f : expf(l[r][i] - m);
+        total += c[r][i];
       }
     }
-    const float inv = 1.f / total;
-    lse_out = m + logf(total);
+    lse_out[r] = -INFINITY;
+    if (m != -INFINITY) {
+      const float inv = 1.f / total;
+      lse_out[r] = m + logf(total);
 #pragma unroll
-    for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i) {
-      if (i < p.n_parts && w[i] != 0.f) {
-        const float4 o = reinterpret_cast<const float4*>(p.o[i] + row * kHeadDim)[lane];
-        const float c = w[i] * inv;
-        acc.x += c * o.x;
-        acc.y += c * o.y;
-        acc.z += c * o.z;
-        acc.w += c * o.w;
+      for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i)
+        if (i < p.n_parts) c[r][i] *= inv;
+    }
+  }
+  f32x4 acc[kRowsPerGroup];
+#pragma unroll
+  for (int r = 0; r < kRowsPerGroup; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i) {
+    if (i < p.n_parts) {
+#pragma unroll
+      for (int r = 0; r < kRowsPerGroup; ++r) {
+        if (c[r][i] != 0.f) {
+          const f32x4 o = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p.o[i] + (row0 + r) * kHeadDim) + lane);
+          acc[r] += c[r][i] * o;
+        }
       }
     }
   }
-  int64_t dst_tok = tok;
-  if (p.restore) dst_tok = (tok < p.first_len) ? p.first_dst + tok : p.second_dst + (tok - p.first_len);
-  const int64_t dst = dst_tok * p.n_heads + head;
-  if (p.out_bf16) {
-    uint2 v;
-    v.x = pack_bf16x2(acc.x, acc.y);
-    v.y = pack_bf16x2(acc.z, acc.w);
-    reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.o_out) + dst * kHeadDim)[lane] = v;
-  } else {
-    reinterpret_cast<float4*>(static_cast<float*>(p.o_out) + dst * kHeadDim)[lane] = acc;
+#pragma unroll
+  for (int r = 0; r < kRowsPerGroup; ++r) {
+    const int64_t row = row0 + r;
+    if (row >= n_rows) break;
+    const int64_t tok = row / p.n_heads;
+    const int head = (int)(row - tok * p.n_heads);
+    int64_t dst_tok = tok;
+    if (p.restore) dst_tok = (tok < p.first_len) ? p.first_dst + tok : p.second_dst + (tok - p.first_len);
+    const int64_t dst = dst_tok * p.n_heads + head;
+    if (p.out_bf16) {
+      uint2 v;
+      v.x = pack_bf16x2(acc[r][0], acc[r][1]);
+      v.y = pack_bf16x2(acc[r][2], acc[r][3]);
+      reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.o_out) + dst * kHeadDim)[lane] = v;
+    } else {
+      __builtin_nontemporal_store(acc[r], reinterpret_cast<f32x4*>(static_cast<float*>(p.o_out) + dst * kHeadDim) + lane);
+    }
+    if (p.lse_out && lane == 0) p.lse_out[dst] = lse_out[r];
   }
-  if (p.lse_out && lane == 0) p.lse_out[dst] = lse_out;
 }
 
 }  // namespace
