@@ -49,9 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
-                    help="before timing, copy this many MiB once with lse_merge_kernel over a single "
-                         "partial (plain float4 loads and stores), so that a counter profile of the run "
-                         "can scale FETCH_SIZE/WRITE_SIZE by a known size")
+                    help="before timing, copy this many MiB once with repartition_kernel (plain "
+                         "16-byte loads and stores), so that a counter profile of the run can scale "
+                         "FETCH_SIZE/WRITE_SIZE by a known size")
     return ap.parse_args()
 
 
@@ -136,15 +136,15 @@ def main():
 
     ws = torch.empty(max(256, cp.workspace_size(make_descs(plan), Hq, Hkv)), dtype=torch.uint8, device=dev)
     if args.copy_calibration_mib > 0:
-        # n_tok rows of 128 fp32 + one fp32 LSE each: (512 + 4) * n_tok bytes in, the same out.
-        n_tok = (args.copy_calibration_mib << 20) // (4 * D)
-        src = torch.ones((n_tok, 1, D), dtype=torch.float32, device=dev)
-        src_l = torch.zeros((n_tok, 1), dtype=torch.float32, device=dev)
+        # A plain copy of known size (repartition_kernel from degree 1 to degree 1:
+        # every row read once and written once with ordinary 16-byte loads and
+        # stores), so that a counter profile can scale FETCH_SIZE/WRITE_SIZE.
+        n_cal = (args.copy_calibration_mib << 20) // (Hkv * D * 2)
+        src = torch.ones((n_cal, Hkv, D), dtype=torch.bfloat16, device=dev)
         dst = torch.empty_like(src)
-        dst_l = torch.empty_like(src_l)
-        cp.attn_merge([src], [src_l], dst, dst_l)
+        cp.repartition(0, n_cal, [src], 1, 0, dst)
         torch.cuda.synchronize()
-        del src, src_l, dst, dst_l
+        del src, dst
     stream = torch.cuda.current_stream()
     flop = 4.0 * D * Hq * plan.visible_pairs
 
