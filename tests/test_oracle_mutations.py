@@ -9,6 +9,7 @@ through.
 import os
 import types
 
+import numpy as np
 import pytest
 
 import oracle_pins as pins
@@ -97,7 +98,9 @@ def test_cache_mutation_is_caught(name, old, new):
 def test_attention_mutation_is_caught(name, old, new):
     from oracle import plan
     att = _mutant("attention.py", old, new)
-    assert _all_pins(att, plan) >= 1, f"no pin catches: {name}"
+    # A mutant may produce -inf or NaN where the pins subtract: expected here.
+    with np.errstate(invalid="ignore"):
+        assert _all_pins(att, plan) >= 1, f"no pin catches: {name}"
 
 
 @pytest.mark.parametrize("name,old,new", PLAN_MUTATIONS, ids=[m[0] for m in PLAN_MUTATIONS])
