@@ -148,9 +148,10 @@ def test_explicit_softmax_scale():
     compare(f64(o), f64(lse), Or, Lr, "scale 0.05")
 
 
-def test_merge_kernel_matches_oracle_merge():
-    g = torch.Generator().manual_seed(41)
-    n_tok, H = 300, 6
+@pytest.mark.parametrize("n_tok,H", [(300, 6), (301, 3)])
+def test_merge_kernel_matches_oracle_merge(n_tok, H):
+    # (301, 3): an odd number of rows, so the last two-row group has one row.
+    g = torch.Generator().manual_seed(41 + n_tok)
     for n in (1, 2, 3, 8, 16):
         outs = [torch.randn(n_tok, H, 128, generator=g) for _ in range(n)]
         lses = [torch.randn(n_tok, H, generator=g) * 4 for _ in range(n)]
