@@ -92,11 +92,18 @@ def fit_prefill_model(samples: Iterable[Tuple[int, int, int, float]]) -> Prefill
 
 
 def measure_attention(grid: Sequence[Tuple[int, int, int]], n_heads_q: int = 32, n_heads_kv: int = 8,
-                      reps: int = 5, seed: int = 0) -> List[Tuple[int, int, int, float]]:
+                      reps: int = 5, seed: int = 0, warmup: int = 3,
+                      warmup_seconds: float = 1.0) -> List[Tuple[int, int, int, float]]:
     """GPU time (seconds) of one attention layer's CP step for each (C, R, P):
     every rank's partial over all its visible keys (prefix through a paged
     cache), each rank timed alone with HIP events on the launch stream; the
-    step time is the slowest rank's (median of ``reps`` runs)."""
+    step time is the slowest rank's (median of ``reps`` runs, after
+    ``warmup`` untimed launches).  The first grid point is also run untimed
+    for ``warmup_seconds`` before anything is measured: a cold GPU (clocks
+    still rising, fresh allocations) measured up to 20% slow on the first
+    points of a grid."""
+    import time
+
     import torch
 
     from . import cpattn as cp
@@ -106,6 +113,7 @@ def measure_attention(grid: Sequence[Tuple[int, int, int]], n_heads_q: int = 32,
     stream = torch.cuda.current_stream()
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
+    warm_left = float(warmup_seconds)
     out = []
     for C, R, P in grid:
         if P % B:
@@ -129,7 +137,14 @@ def measure_attention(grid: Sequence[Tuple[int, int, int]], n_heads_q: int = 32,
             desc = cp.make_desc(plan, q, k, v, o, lse, kc, vc, table, include_prefix=True)
             ws = torch.empty(max(256, cp.workspace_size([desc], n_heads_q, n_heads_kv)), dtype=torch.uint8,
                              device=dev)
-            cp.attn_partial([desc], n_heads_q, n_heads_kv, ws, stream=stream)
+            for _ in range(max(1, warmup)):
+                cp.attn_partial([desc], n_heads_q, n_heads_kv, ws, stream=stream)
+            if warm_left > 0:
+                t_end = time.perf_counter() + warm_left
+                while time.perf_counter() < t_end:
+                    cp.attn_partial([desc], n_heads_q, n_heads_kv, ws, stream=stream)
+                    torch.cuda.synchronize()
+                warm_left = 0.0
             times = []
             for _ in range(reps):
                 a = torch.cuda.Event(enable_timing=True)
