@@ -228,6 +228,18 @@ def main():
     rp_bytes = 2 * 2 * R * Hkv * D * 2                # K and V rows, read once and written once
     del k_ranks, v_ranks, dst_k, dst_v, k_store, v_store
 
+    # The paged gather on its own: a 48K-token cached prefix (the prefix-hit
+    # workload's, 3072 blocks of 16 under a permuted table) read back out of
+    # the paged cache into contiguous K and V rows, one launch.
+    P_g = synth.WORKLOADS["prefix_hit_64k_c2"].P
+    pre_g = synth.paged_prefix(gen, P_g, Hkv, D, 1.0, spare_blocks=64, device="cuda")
+    k_g = torch.empty((P_g, Hkv, D), dtype=torch.bfloat16, device=dev)
+    v_g = torch.empty_like(k_g)
+    ga_ms = timed(lambda: cp.kv_gather(pre_g.k_cache, pre_g.v_cache, pre_g.block_table, 0, k_g, v_g,
+                                       stream=stream))
+    ga_bytes = 2 * 2 * P_g * Hkv * D * 2             # K and V rows, read once and written once
+    del pre_g, k_g, v_g
+
     # --- CPU oracle on a bounded sample of the same rows ----------------------
     cpu = None
     parity = None
@@ -275,6 +287,12 @@ def main():
             "GB_s": round(wb_bytes / (wb_ms * 1e-3) / 1e9, 1),
             "frac": round(wb_bytes / (wb_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "what": "every rank's new K and V rows into the block-16 paged cache (C launches)",
+        },
+        "paged_gather": {
+            "kernel": "kv_gather_kernel", "bound": "hbm", "ms": round(ga_ms, 4), "bytes": ga_bytes,
+            "GB_s": round(ga_bytes / (ga_ms * 1e-3) / 1e9, 1),
+            "frac": round(ga_bytes / (ga_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "what": "a 49152-token paged prefix (permuted block-16 table) read back into contiguous K and V rows",
         },
         "repartition": {
             "kernel": "repartition_kernel", "bound": "hbm", "ms": round(rp_ms, 4), "bytes": rp_bytes,

@@ -15,7 +15,8 @@
  *   Sec. 7.1  The cached prefix is a sequence of fixed-size cache blocks.
  *   Sec. 6.2, 7.2  After a worker split or merge, and for replication between
  *             workers of different CP degree, resident KV is re-sharded to
- *             the destination's CP geometry.
+ *             the destination's CP geometry (and read out of the paged
+ *             cache for the destination).
  *
  * Conventions shared by every call:
  *   - Tensors are dense, row-major, in device memory unless a pointer is
@@ -266,6 +267,31 @@ int cp_kv_writeback(const cp_rank_plan* plan, const void* k_rows, const void* v_
  */
 int cp_repartition(int64_t P, int64_t R, int32_t C_src, const void* const* src_rows, int32_t C_dst,
                    int32_t dst_rank, void* dst_rows, int64_t row_bytes, void* stream);
+
+/*
+ * Paged KV gather: copies positions pos_begin .. pos_begin + n_tokens - 1 of
+ * one request out of the block-16 paged cache into contiguous rows.  It is
+ * the read side of cp_kv_writeback and the same block-table gather that
+ * cp_attn_partial performs tile by tile for a cached prefix (Sec. 2.2: a
+ * prefix hit reuses the cached KV states; Sec. 7.1: one trie node is one
+ * cache block), here as a standalone copy -- e.g. the KV states handed to a
+ * worker of another CP degree on replication (Sec. 7.2).
+ *   k_cache, v_cache  bf16 device [n_blocks][16][n_heads_kv][head_dim].
+ *   block_table int32 device [table_len]: position p lives in block
+ *               block_table[p / 16], slot p % 16; table_len must cover the
+ *               range: table_len >= ceil((pos_begin + n_tokens) / 16).
+ *   k_rows, v_rows  bf16 device [n_tokens][n_heads_kv][head_dim], written:
+ *               row t is position pos_begin + t.  16-byte aligned; must not
+ *               overlap the caches.
+ *   n_heads_kv, head_dim  Hkv >= 1; head_dim a positive multiple of 8.
+ * A row whose block-table entry lies outside [0, n_blocks) is written as
+ * zeros (nothing is read through such an entry).  n_tokens == 0 is a no-op.
+ * Errors: CP_ERR_INVALID (pointers, alignment, shapes, negative counts,
+ * table_len), CP_ERR_UNSUPPORTED (positions beyond 2^31), CP_ERR_HIP.
+ */
+int cp_kv_gather(const void* k_cache, const void* v_cache, int64_t n_blocks, const int32_t* block_table,
+                 int64_t table_len, int64_t pos_begin, int64_t n_tokens, int32_t n_heads_kv,
+                 int32_t head_dim, void* k_rows, void* v_rows, void* stream);
 
 #ifdef __cplusplus
 }

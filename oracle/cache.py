@@ -1,5 +1,6 @@
-"""Oracle: the KV-cache steps after the attention -- writing a request's new
-K/V into the paged prefix cache, and re-sharding rows between CP degrees.
+"""Oracle: the KV-cache steps around the attention -- writing a request's new
+K/V into the paged prefix cache, reading positions back out of it, and
+re-sharding rows between CP degrees.
 
 TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
@@ -12,6 +13,10 @@ Definitions followed:
   block ``block_table[p // 16]``, slot ``p % 16`` -- the same addressing the
   prefix gather (``attention.gather_paged``) reads.  Every other slot keeps
   what it held.
+* Read-back (Sec. 2.2: a prefix hit reuses the cached KV states; Sec. 7.1: one
+  trie node is one cache block; Sec. 7.2: replication hands KV states to
+  another worker).  The row of position p is the one ``write_paged`` stored at
+  ``block_table[p // 16]``, slot ``p % 16``.
 * Re-sharding between CP degrees (Sec. 6.2: after a split or merge the
   resident KV blocks are installed under the new CP geometry; Sec. 7.2:
   inter-degree replication repartitions KV states for the destination
@@ -50,6 +55,26 @@ def write_paged(cache, block_table, positions, rows, block_tokens=BLOCK_TOKENS):
         raise ValueError("two rows for one position")
     for i, p in enumerate(positions):
         out[table[int(p) // block_tokens], int(p) % block_tokens] = rows[i]
+    return out
+
+
+def read_paged(cache, block_table, pos_begin, n, block_tokens=BLOCK_TOKENS):
+    """Rows of positions pos_begin .. pos_begin + n - 1 read out of a paged
+    cache: position p is held in physical block ``block_table[p // block_tokens]``,
+    slot ``p % block_tokens`` (the addressing ``write_paged`` stores through).
+    A position whose block-table entry lies outside the cache reads as zeros
+    (reading: nothing is read through such an entry).
+
+    cache: [n_blocks, block_tokens, ...]; returns [n, ...].
+    """
+    cache = np.asarray(cache)
+    table = np.asarray(block_table, dtype=np.int64)
+    out = np.zeros((n,) + cache.shape[2:], dtype=cache.dtype)
+    for t in range(n):
+        p = pos_begin + t
+        blk = table[p // block_tokens]
+        if 0 <= blk < cache.shape[0]:
+            out[t] = cache[blk, p % block_tokens]
     return out
 
 

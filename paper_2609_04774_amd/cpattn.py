@@ -30,7 +30,7 @@ CP_MAX_DEGREE = 64
 
 EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
             "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_merge",
-            "cp_kv_writeback", "cp_repartition")
+            "cp_kv_writeback", "cp_repartition", "cp_kv_gather")
 
 
 class CpChunk(ctypes.Structure):
@@ -109,6 +109,10 @@ def _load():
     lib.cp_repartition.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                    ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_int32,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.cp_kv_gather.restype = ctypes.c_int
+    lib.cp_kv_gather.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                 ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     return lib
 
 
@@ -245,6 +249,16 @@ def kv_writeback(plan: CpRankPlan, k_rows, v_rows, k_cache, v_cache, block_table
     _check(lib.cp_kv_writeback(ctypes.byref(plan), _ptr(k_rows), _ptr(v_rows), Hkv, D, _ptr(k_cache),
                                _ptr(v_cache), n_blocks, _ptr(block_table), block_table.numel(),
                                _stream_handle(stream)))
+
+
+def kv_gather(k_cache, v_cache, block_table, pos_begin: int, k_rows, v_rows, stream=None):
+    """cp_kv_gather of torch device tensors: positions pos_begin ..
+    pos_begin + len(k_rows) - 1 out of caches [n_blocks, 16, Hkv, D] through
+    block_table into k_rows, v_rows [n, Hkv, D]."""
+    n_blocks, _, Hkv, D = k_cache.shape
+    _check(lib.cp_kv_gather(_ptr(k_cache), _ptr(v_cache), n_blocks, _ptr(block_table), block_table.numel(),
+                            pos_begin, k_rows.shape[0], Hkv, D, _ptr(k_rows), _ptr(v_rows),
+                            _stream_handle(stream)))
 
 
 def repartition(prefix_len: int, new_len: int, src_rows, C_dst: int, dst_rank: int, dst_rows, stream=None):

@@ -125,7 +125,8 @@ struct MergeParams {
 int launch_merge(const MergeParams& p, void* stream);
 
 // ---------------------------------------------------------------------------
-// KV-cache steps after the attention: paged write-back and re-sharding.
+// KV-cache steps after the attention: paged write-back, re-sharding and the
+// paged gather.
 
 struct WritebackParams {
   const unsigned char* k_rows;  // [n_rows][row_bytes]
@@ -155,5 +156,19 @@ struct RepartitionParams {
 };
 
 int launch_repartition(const RepartitionParams& p, void* stream);
+
+struct GatherParams {
+  const unsigned char* k_cache;  // [n_blocks][16][row_bytes]
+  const unsigned char* v_cache;
+  const int32_t* block_table;
+  int64_t n_blocks;
+  int64_t row_bytes;             // Hkv * D * 2, a multiple of 16
+  int64_t pos_begin;             // position of output row 0
+  int64_t n_rows;
+  unsigned char* k_rows;         // [n_rows][row_bytes]
+  unsigned char* v_rows;
+};
+
+int launch_gather(const GatherParams& p, void* stream);
 
 }  // namespace cpattn

@@ -1,5 +1,6 @@
 // Host side of the KV-cache steps after the attention: argument checks and
-// kernel parameters for cp_kv_writeback and cp_repartition (include/cp_attn.h).
+// kernel parameters for cp_kv_writeback, cp_repartition and cp_kv_gather
+// (include/cp_attn.h).
 #include <cstdint>
 #include <cstring>
 #include <string>
@@ -94,6 +95,40 @@ extern "C" int cp_repartition(int64_t P, int64_t R, int32_t C_src, const void* c
   }
   p.n_rows = dst.n_rows;
   const int st = launch_repartition(p, stream);
+  if (st == CP_OK) clear_error();
+  return st;
+}
+
+extern "C" int cp_kv_gather(const void* k_cache, const void* v_cache, int64_t n_blocks, const int32_t* block_table,
+                            int64_t table_len, int64_t pos_begin, int64_t n_tokens, int32_t n_heads_kv,
+                            int32_t head_dim, void* k_rows, void* v_rows, void* stream) {
+  const std::string who = "cp_kv_gather: ";
+  if (pos_begin < 0 || n_tokens < 0) return fail(CP_ERR_INVALID, who + "pos_begin and n_tokens must be >= 0");
+  if (pos_begin + n_tokens > ((int64_t)1 << 31)) return fail(CP_ERR_UNSUPPORTED, who + "positions beyond 2^31");
+  if (n_heads_kv < 1 || head_dim < 8 || head_dim % 8)
+    return fail(CP_ERR_INVALID, who + "n_heads_kv must be >= 1 and head_dim a positive multiple of 8");
+  if (n_blocks < 0) return fail(CP_ERR_INVALID, who + "n_blocks < 0");
+  if (table_len < (pos_begin + n_tokens + CP_KV_BLOCK_TOKENS - 1) / CP_KV_BLOCK_TOKENS)
+    return fail(CP_ERR_INVALID, who + "block table shorter than ceil((pos_begin + n_tokens) / 16)");
+  if (n_tokens > 0) {
+    if (!k_rows || !v_rows || !k_cache || !v_cache || !block_table)
+      return fail(CP_ERR_INVALID, who + "rows, caches and block table are required");
+    if (!aligned(k_rows, 16) || !aligned(v_rows, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+        !aligned(block_table, 4))
+      return fail(CP_ERR_INVALID, who + "rows/caches must be 16-byte and the block table 4-byte aligned");
+  }
+  GatherParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.k_cache = static_cast<const unsigned char*>(k_cache);
+  p.v_cache = static_cast<const unsigned char*>(v_cache);
+  p.block_table = block_table;
+  p.n_blocks = n_blocks;
+  p.row_bytes = (int64_t)n_heads_kv * head_dim * 2;
+  p.pos_begin = pos_begin;
+  p.n_rows = n_tokens;
+  p.k_rows = static_cast<unsigned char*>(k_rows);
+  p.v_rows = static_cast<unsigned char*>(v_rows);
+  const int st = launch_gather(p, stream);
   if (st == CP_OK) clear_error();
   return st;
 }

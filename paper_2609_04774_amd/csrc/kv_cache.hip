@@ -1,4 +1,4 @@
-// KV-cache steps after the attention, both pure row copies (HBM-bound):
+// KV-cache steps around the attention, all pure row copies (HBM-bound):
 //
 //  * Paged write-back (paper Sec. 2.2, 7.1, 8): a CP rank's new K/V rows go
 //    to their token positions in the block-16 paged cache, position p at
@@ -6,6 +6,8 @@
 //  * Re-sharding between CP degrees (Sec. 6.2, 7.2): each row of a
 //    destination rank is fetched from the source rank that holds the same
 //    global position under the source degree.
+//  * Paged gather (Sec. 2.2, 7.1, 7.2): positions of a request read back out
+//    of the paged cache into contiguous rows.
 //
 // A workgroup takes 4 rows, one wave per row; each lane moves
 // 16-byte pieces with plain vector loads and stores, so a row's bytes are
@@ -84,7 +86,61 @@ __global__ __launch_bounds__(kThreads) void repartition_kernel(RepartitionParams
   }
 }
 
+// One wave gathers one row of K and one of V out of the paged cache: per
+// round, up to four 16-byte pieces of each (lane l takes pieces l, l+64, ...)
+// are loaded before any is stored, with non-temporal hints (every byte is
+// moved once).  A NULL source (a block-table entry outside the cache) writes
+// zeros.
+__device__ __forceinline__ void gather_row_pair(const unsigned char* ks, const unsigned char* vs,
+                                                unsigned char* kd, unsigned char* vd, int64_t row_bytes,
+                                                int lane) {
+  const int64_t n = row_bytes >> 4;
+  for (int64_t base = 0; base < n; base += 4 * 64) {
+    u32x4 kv[4], vv[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t i = base + lane + 64 * k;
+      kv[k] = vv[k] = u32x4{0u, 0u, 0u, 0u};
+      if (i < n && ks) {
+        kv[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ks) + i);
+        vv[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vs) + i);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t i = base + lane + 64 * k;
+      if (i < n) {
+        __builtin_nontemporal_store(kv[k], reinterpret_cast<u32x4*>(kd) + i);
+        __builtin_nontemporal_store(vv[k], reinterpret_cast<u32x4*>(vd) + i);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void kv_gather_kernel(GatherParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int k = wave; k < kRowsPerGroup; k += kWaves) {
+    const int64_t t = (int64_t)blockIdx.x * kRowsPerGroup + k;
+    if (t >= p.n_rows) break;
+    const int64_t pos = p.pos_begin + t;
+    const int64_t blk = p.block_table[pos / kBlockTokens];
+    const bool inside = blk >= 0 && blk < p.n_blocks;
+    const int64_t src = (blk * kBlockTokens + pos % kBlockTokens) * p.row_bytes;
+    gather_row_pair(inside ? p.k_cache + src : nullptr, inside ? p.v_cache + src : nullptr,
+                    p.k_rows + t * p.row_bytes, p.v_rows + t * p.row_bytes, p.row_bytes, lane);
+  }
+}
+
 }  // namespace
+
+int launch_gather(const GatherParams& p, void* stream) {
+  if (p.n_rows == 0) return CP_OK;
+  const int64_t groups = (p.n_rows + kRowsPerGroup - 1) / kRowsPerGroup;
+  hipLaunchKernelGGL(kv_gather_kernel, dim3((unsigned)groups), dim3(kThreads), 0, (hipStream_t)stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_kv_gather launch: ") + hipGetErrorString(e));
+  return CP_OK;
+}
 
 int launch_writeback(const WritebackParams& p, void* stream) {
   if (p.n_rows == 0) return CP_OK;

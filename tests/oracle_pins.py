@@ -215,6 +215,31 @@ def check_plan(shard_plan, remaining_workload, shard_plan_fast=None):
         assert sorted(seen) == list(range(P, P + R)), "rows are not a bijection onto the suffix"
 
 
+def check_read_paged(read_paged, write_paged, seed=12):
+    """Paged read-back (Sec. 2.2, 7.1, 7.2): addressing by hand; an identity
+    block table reads the cache in storage order (closed form); reading a
+    range back after writing it returns the rows written, from any start
+    position; entries outside the cache read as zeros."""
+    cache = np.arange(5 * 16, dtype=np.float64).reshape(5, 16, 1, 1)
+    got = read_paged(cache, [4, 0, 2], 15, 4)                 # positions 15, 16, 17, 18
+    assert got.reshape(-1).tolist() == [4 * 16 + 15, 0, 1, 2], "block/slot addressing"
+    rng = _rng(seed)
+    Hkv, D, B = 2, 4, 16
+    nb = 7
+    cache = rng.standard_normal((nb, B, Hkv, D))
+    assert np.array_equal(read_paged(cache, np.arange(nb), 0, nb * B), cache.reshape(nb * B, Hkv, D)), \
+        "identity table must read the cache in order"
+    for start, n in [(0, 50), (13, 40), (16, 16), (31, 1), (5, 0)]:
+        table = rng.permutation(nb + 3)[:nb]
+        x = rng.standard_normal((n, Hkv, D))
+        written = write_paged(np.full((nb + 3, B, Hkv, D), np.nan), table, list(range(start, start + n)), x)
+        assert np.array_equal(read_paged(written, table, start, n), x), "read-back of written rows"
+    bad = np.array([1, -1, 9, 0])
+    out = read_paged(cache, bad, 0, 4 * B)
+    assert np.array_equal(out[:B], cache[1]) and np.array_equal(out[3 * B:], cache[0]), "valid entries"
+    assert not np.any(out[B:3 * B]), "entries outside the cache read as zeros"
+
+
 def check_writeback(write_paged, rank_writeback, gather_paged, seed=9):
     """Write-back into the paged cache (Sec. 2.2, 7.1, 8): the addressing by
     hand, the round trip through the prefix gather (itself pinned by

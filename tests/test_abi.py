@@ -260,6 +260,27 @@ def test_writeback_argument_errors():
     assert cp.last_error() != ""
 
 
+def _ga_status(cache=FAKE, n_blocks=8, table=FAKE, table_len=5, pos_begin=8, n=70, Hkv=2, D=128, rows=FAKE):
+    return cp.lib.cp_kv_gather(cache, cache, n_blocks, table, table_len, pos_begin, n, Hkv, D, rows, rows, None)
+
+
+def test_gather_argument_errors():
+    assert _ga_status(table_len=4) == cp.CP_ERR_INVALID               # positions 8..77 need 5 blocks
+    assert _ga_status(rows=None) == cp.CP_ERR_INVALID
+    assert _ga_status(cache=None) == cp.CP_ERR_INVALID
+    assert _ga_status(cache=FAKE + 8) == cp.CP_ERR_INVALID
+    assert _ga_status(table=FAKE + 2) == cp.CP_ERR_INVALID
+    assert _ga_status(Hkv=0) == cp.CP_ERR_INVALID
+    assert _ga_status(D=12) == cp.CP_ERR_INVALID
+    assert _ga_status(n_blocks=-1) == cp.CP_ERR_INVALID
+    assert _ga_status(pos_begin=-1) == cp.CP_ERR_INVALID
+    assert _ga_status(n=-1) == cp.CP_ERR_INVALID
+    assert _ga_status(pos_begin=1 << 31, table_len=1 << 28) == cp.CP_ERR_UNSUPPORTED
+    assert cp.last_error() != ""
+    # Nothing to copy: no pointer is needed and nothing is launched.
+    assert _ga_status(cache=None, table=None, rows=None, n=0, table_len=1) == cp.CP_OK
+
+
 def _rp_status(P=0, R=64, C_src=2, C_dst=4, dst_rank=0, src=None, dst=FAKE, row_bytes=4096):
     ptrs = (ctypes.c_void_p * max(1, C_src))(*([FAKE * 2] * C_src if src is None else src))
     return cp.lib.cp_repartition(P, R, C_src, ptrs, C_dst, dst_rank, dst, row_bytes, None)

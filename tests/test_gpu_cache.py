@@ -168,3 +168,51 @@ def test_repartition_full_size_round_trip():
         cp.repartition(0, w.R, mid, 4, r, back)
         torch.cuda.synchronize()
         assert torch.equal(back, src[r])
+
+
+@pytest.mark.parametrize("pos_begin,n,Hkv", [(0, 100, 2), (37, 70, 1), (16, 16, 8), (5, 1, 4), (0, 0, 2)])
+def test_gather_matches_oracle(pos_begin, n, Hkv):
+    g = synth.generator(3600 + pos_begin + n, device=DEV)
+    D = 128
+    table, kc, vc = _request_cache(g, 0, pos_begin + n, Hkv, D, spare=4)
+    k = torch.full((n, Hkv, D), float("nan"), dtype=torch.bfloat16, device=DEV)
+    v = torch.full((n, Hkv, D), float("nan"), dtype=torch.bfloat16, device=DEV)
+    cp.kv_gather(kc, vc, table, pos_begin, k, v)
+    torch.cuda.synchronize()
+    tab = table.cpu().numpy()
+    assert np.array_equal(f64(k), ocache.read_paged(f64(kc), tab, pos_begin, n))
+    assert np.array_equal(f64(v), ocache.read_paged(f64(vc), tab, pos_begin, n))
+
+
+def test_gather_of_entries_outside_the_cache_is_zero():
+    g = synth.generator(3700, device=DEV)
+    Hkv, D, n = 2, 128, 64
+    table, kc, vc = _request_cache(g, 0, n, Hkv, D, spare=0)
+    bad = table.clone()
+    bad[1] = kc.shape[0]
+    bad[2] = -7
+    k = torch.full((n, Hkv, D), float("nan"), dtype=torch.bfloat16, device=DEV)
+    v = torch.full_like(k, float("nan"))
+    cp.kv_gather(kc, vc, bad, 0, k, v)
+    torch.cuda.synchronize()
+    tab = bad.cpu().numpy()
+    assert np.array_equal(f64(k), ocache.read_paged(f64(kc), tab, 0, n))
+    assert np.array_equal(f64(v), ocache.read_paged(f64(vc), tab, 0, n))
+    assert not torch.any(k[16:48].float()) and not torch.any(v[16:48].float())
+
+
+def test_gather_full_size_round_trip():
+    """The 48K-token prefix of the prefix-hit workload (3072 blocks of 16,
+    permuted table, Llama-3-8B KV heads) read back out of the paged cache is
+    exactly what the cache holds at those positions."""
+    w = synth.WORKLOADS["prefix_hit_64k_c2"]
+    g = synth.generator(3800, device=DEV)
+    pre = synth.paged_prefix(g, w.P, w.Hkv, w.D, 1.0, spare_blocks=16, device=DEV)
+    k = torch.empty((w.P, w.Hkv, w.D), dtype=torch.bfloat16, device=DEV)
+    v = torch.empty_like(k)
+    cp.kv_gather(pre.k_cache, pre.v_cache, pre.block_table, 0, k, v)
+    torch.cuda.synchronize()
+    pos = torch.arange(w.P, device=DEV)
+    idx = pre.block_table.long()[pos // B] * B + pos % B
+    assert torch.equal(k, pre.k_cache.reshape(-1, w.Hkv, w.D)[idx])
+    assert torch.equal(v, pre.v_cache.reshape(-1, w.Hkv, w.D)[idx])

@@ -130,5 +130,9 @@ def test_paged_writeback_round_trip():
     pins.check_writeback(ocache.write_paged, ocache.rank_writeback, oatt.gather_paged)
 
 
+def test_paged_read_back():
+    pins.check_read_paged(ocache.read_paged, ocache.write_paged)
+
+
 def test_repartition_between_degrees():
     pins.check_repartition(ocache.repartition)

@@ -33,6 +33,7 @@ def _all_pins(att, plan, cache=None):
     checks = [
         lambda: pins.check_writeback(cache.write_paged, cache.rank_writeback, att.gather_paged),
         lambda: pins.check_repartition(cache.repartition),
+        lambda: pins.check_read_paged(cache.read_paged, cache.write_paged),
         lambda: pins.check_brute(att.attend),
         lambda: pins.check_sdpa(att.full_causal_attention),
         lambda: pins.check_closed_forms(att.full_causal_attention),
@@ -84,6 +85,9 @@ CACHE_MUTATIONS = [
     ("repartition reads the destination's own plan", "plan = shard_plan_fast(P, R, C_src, r)",
      "plan = shard_plan_fast(P, R, C_dst, r) if r < C_dst else shard_plan_fast(P, R, C_src, r)"),
     ("repartition reverses a rank's rows", "where[pos] = (r, t)", "where[pos] = (r, plan[\"n_rows\"] - 1 - t)"),
+    ("read-back ignores pos_begin", "p = pos_begin + t", "p = t"),
+    ("read-back slot off by one", "out[t] = cache[blk, p % block_tokens]", "out[t] = cache[blk, (p + 1) % block_tokens]"),
+    ("read-back of a bad entry wraps", "if 0 <= blk < cache.shape[0]:", "if True:"),
 ]
 
 
