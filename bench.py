@@ -55,9 +55,10 @@ def parse():
     return ap.parse_args()
 
 
-def measured_traffic(workload):
-    """HBM bytes per attention launch from the committed counter profile of
-    this workload, if the kernel source is still the one that was profiled."""
+def profiled_figures(workload):
+    """Figures of the committed counter profile of this workload (HBM bytes
+    per attention launch, and where recorded the clock and MFMA-busy
+    fraction), if the kernel source is still the one that was profiled."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     src = os.path.join(ROOT, "paper_2609_04774_amd", "csrc", "attn_partial.hip")
@@ -73,7 +74,29 @@ def measured_traffic(workload):
         sha = hashlib.sha256(f.read()).hexdigest()
     if kv.get("kernel_source_sha256") != sha:
         return None
-    return int(kv["fetch_bytes"]) + int(kv["write_bytes"])
+    out = {"traffic": int(kv["fetch_bytes"]) + int(kv["write_bytes"])}
+    if "clock_ghz" in kv and "mfma_busy" in kv:
+        out["clock_ghz"] = float(kv["clock_ghz"])
+        out["mfma_busy"] = float(kv["mfma_busy"])
+    return out
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the committed counter profile."""
+    f = profiled_figures(workload)
+    return None if f is None else f["traffic"]
+
+
+def counter_profile(workload, args, rank):
+    """The committed counter profile's clock and MFMA-busy fraction for this
+    launch configuration (null when there is none for the current source)."""
+    if args.mode != "passkv" or rank != 0:
+        return None
+    f = profiled_figures(workload)
+    if f is None or "clock_ghz" not in f:
+        return None
+    return {"clock_ghz": f["clock_ghz"], "mfma_busy": f["mfma_busy"],
+            "source": f"profiles/traffic_{workload}.txt (rocprofv3 GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES)"}
 
 
 def main():
@@ -276,6 +299,7 @@ def main():
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": measured_traffic(w.name) if args.mode == "passkv" and rank == 0 else None,
             "launch_ms": round(attn_ms, 4),
+            "profiled": counter_profile(w.name, args, rank),
         },
         "merge": {
             "kernel": "lse_merge_kernel", "bound": "hbm", "ms": round(merge_ms, 4),
