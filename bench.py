@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--rank", type=int, default=0)
     ap.add_argument("--mode", choices=["passkv", "allgather"], default="passkv")
+    ap.add_argument("--no-hetero", dest="hetero", action="store_false",
+                    help="skip the heterogeneous-batch (varlen launch) measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -85,6 +87,68 @@ def measured_traffic(workload):
     """HBM bytes per attention launch from the committed counter profile."""
     f = profiled_figures(workload)
     return None if f is None else f["traffic"]
+
+
+def heterogeneous_batch(args, gen, dev, stream, reps=5):
+    """The varlen launch: 64 requests of lognormal length (median 2048, clipped
+    to 256..131072), each with its CP degree by length bucket, 19 of them with
+    a cached prefix in one shared paged pool -- every (request, rank) shard's
+    partial over all its visible keys in one cp_attn_partial launch."""
+    import torch
+
+    import synth
+    from paper_2609_04774_amd import cpattn as cp
+
+    Hq, Hkv, D, B = 32, 8, 128, synth.BLOCK_TOKENS
+    reqs = synth.hetero_requests()
+    total_blocks = sum(P // B for _, P, _ in reqs) + 32
+    k_pool = synth.randn_bf16(gen, (total_blocks, B, Hkv, D), device="cuda")
+    v_pool = synth.randn_bf16(gen, (total_blocks, B, Hkv, D), device="cuda")
+    free = torch.randperm(total_blocks, generator=gen, device="cuda")
+    used = 0
+    keep, descs = [], []
+    pairs = 0
+    for L, P, C in reqs:
+        R = L - P
+        k = synth.randn_bf16(gen, (R, Hkv, D), device="cuda")
+        v = synth.randn_bf16(gen, (R, Hkv, D), device="cuda")
+        table = None
+        if P:
+            pre = synth.paged_prefix(gen, P, Hkv, D, device="cuda",
+                                     pool=(k_pool, v_pool, free[used:used + P // B]))
+            used += P // B
+            table = pre.block_table
+        for r in range(C):
+            plan, _ = cp.shard_plan(P, R, C, r, with_rows=False)
+            if plan.n_rows == 0:
+                continue
+            q = synth.randn_bf16(gen, (plan.n_rows, Hq, D), device="cuda")
+            o = torch.empty((plan.n_rows, Hq, D), dtype=torch.float32, device=dev)
+            lse = torch.empty((plan.n_rows, Hq), dtype=torch.float32, device=dev)
+            descs.append(cp.make_desc(plan, q, k, v, o, lse, k_pool, v_pool, table, include_prefix=True))
+            keep.append((q, k, v, o, lse))
+            pairs += plan.visible_pairs
+    ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=dev)
+    for _ in range(2):
+        cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flop = 4.0 * D * Hq * pairs
+    out = {
+        "kernel": "attn_partial_kernel", "requests": len(reqs), "tokens": sum(L for L, _, _ in reqs),
+        "prefixed": sum(1 for _, P, _ in reqs if P), "descriptors": len(descs), "flop": flop,
+        "ms": round(ms, 4), "TFLOP_s": round(flop / (ms * 1e-3) / 1e12, 2),
+        "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+    }
+    del keep, descs, ws, k_pool, v_pool
+    return out
 
 
 def counter_profile(workload, args, rank):
@@ -263,6 +327,8 @@ def main():
     ga_bytes = 2 * 2 * P_g * Hkv * D * 2             # K and V rows, read once and written once
     del pre_g, k_g, v_g
 
+    hetero = heterogeneous_batch(args, gen, dev, stream) if args.hetero else None
+
     # --- CPU oracle on a bounded sample of the same rows ----------------------
     cpu = None
     parity = None
@@ -318,6 +384,7 @@ def main():
             "frac": round(ga_bytes / (ga_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "what": "a 49152-token paged prefix (permuted block-16 table) read back into contiguous K and V rows",
         },
+        "heterogeneous_batch": hetero,
         "repartition": {
             "kernel": "repartition_kernel", "bound": "hbm", "ms": round(rp_ms, 4), "bytes": rp_bytes,
             "GB_s": round(rp_bytes / (rp_ms * 1e-3) / 1e9, 1),
