@@ -697,7 +697,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   *reinterpret_cast<u32x4*>(smem + (kBufs + ((t_first + kBufs - 1) & (kBufs - 1))) * kTileBytes + 16 * tid) =
       u32x4{};
   __syncthreads();  // the first tile is in LDS for everyone
-  if (n_tiles > 0) qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
+  if (n_tiles > 0 && wave_active) qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
 
   // Iteration j (tile buffer B = j % kBufs): mask
   // S_j, then the region (S_{j+1} from K buffer B+1, softmax of S_j, P_{j-1}
@@ -705,14 +705,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // B+kAhead), then O's rescale if the max moved.  The last iteration
   // computes scores of the tile after its own from the repeated last tile
   // (finite data, unused).
-  auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
-    const int B = j & (kBufs - 1);
-    if ((j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c) {
-      int lim[kNB];
-      tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
-      mask_tile(s_in, half, lim);
-    }
-    const int t = j + kAhead, buf = (B + kAhead) % kBufs;
+  // This wave's share of the load that iteration j issues (tile j+kAhead).
+  auto next_load = [&](int j) {
+    const int t = j + kAhead, buf = t & (kBufs - 1);
     TileLoad ld;
     if (t >= cur_full) {
       ld = load_of(t, buf);
@@ -725,6 +720,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       ld.lv = lv0 + buf * kTileBytes + wave_dst;
     }
     cur = ld;
+    return ld;
+  };
+  auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
+    const int B = j & (kBufs - 1);
+    if ((j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c) {
+      int lim[kNB];
+      tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
+      mask_tile(s_in, half, lim);
+    }
+    const TileLoad ld = next_load(j);
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
                      pf, o, s_in, s_out, m_run, l_run, lb_run, sl2, ld);
   };
@@ -734,16 +739,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // own); the two tiles issued after those may still be in flight.  After the
   // barrier every wave is also done with the iterations before the pair, the
   // last readers of the buffers its loads reuse (tile j+5 takes tile j-3's).
-  for (int j = t_first; j < t_stop; j += 2) {
-    __builtin_amdgcn_s_waitcnt(kWaitVm(2 * kLoadsPerTile));
-    __syncthreads();
-    iteration(j, sa, sb);
-    if (j + 1 >= t_stop) break;
-    iteration(j + 1, sb, sa);
+  // A wave with no query row in the work item (a query block cut short at a
+  // chunk's end) computes nothing: it only loads its share of every tile and
+  // keeps the workgroup's barriers.
+  if (wave_active) {
+    for (int j = t_first; j < t_stop; j += 2) {
+      __builtin_amdgcn_s_waitcnt(kWaitVm(2 * kLoadsPerTile));
+      __syncthreads();
+      iteration(j, sa, sb);
+      if (j + 1 >= t_stop) break;
+      iteration(j + 1, sb, sa);
+    }
+  } else {
+    for (int j = t_first; j < t_stop; j += 2) {
+      __builtin_amdgcn_s_waitcnt(kWaitVm(2 * kLoadsPerTile));
+      __syncthreads();
+      issue_tile(next_load(j));
+      if (j + 1 >= t_stop) break;
+      issue_tile(next_load(j + 1));
+    }
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
+  if (n_tiles > 0 && wave_active) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
