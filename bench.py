@@ -46,8 +46,9 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--rank", type=int, default=0)
     ap.add_argument("--mode", choices=["passkv", "allgather"], default="passkv")
-    ap.add_argument("--no-hetero", dest="hetero", action="store_false",
-                    help="skip the heterogeneous-batch (varlen launch) measurement")
+    ap.add_argument("--hetero", action="store_true",
+                    help="also time the heterogeneous batch (64 requests, one varlen launch); off by default so "
+                         "that a kernel trace of the default run holds only the workload's attention launches")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
