@@ -3,12 +3,18 @@
 
 A step is one pass of the whole path for rank 0 of the workload:
   1. the zigzag shard plan (host, cp_shard_plan);
-  2. partial attention of the rank's rows against each of the C ranks' KV
-     shards (and the paged prefix, if any) -- one cp_attn_partial launch with
-     C (+1) descriptors;
-  3. the exact LSE merge of those partials, writing each row back to its
-     place in the original sequence order (cp_attn_merge with the plan).
-Inputs are resident in HBM before the timed region starts.
+  2. partial attention of the rank's rows -- one cp_attn_partial launch:
+     by default (--mode allgather) against every key the rank's rows see in
+     the all-gathered KV (and the paged prefix, if any), one descriptor;
+     with --mode passkv against each of the C ranks' KV shards (and the
+     prefix) separately, C (+1) descriptors;
+  3. cp_attn_merge with the plan: the exact LSE merge of the partials (one
+     partial in the all-gather view), writing each row back to its place in
+     the original sequence order.
+Inputs are resident in HBM before the timed region starts.  In the
+all-gather view the merge object reports a separate leg: C (+1) partials of
+the same rows (seeded values, every LSE finite, so every partial is read)
+merged and restored.
 
 value  = 4 * D * Hq * visible_pairs / step time  (TFLOP/s; the two MFMA
          contractions per visible query-key pair, no credit for masked work).
@@ -45,7 +51,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--rank", type=int, default=0)
-    ap.add_argument("--mode", choices=["passkv", "allgather"], default="passkv")
+    ap.add_argument("--mode", choices=["passkv", "allgather"], default="allgather")
     ap.add_argument("--hetero", action="store_true",
                     help="also time the heterogeneous batch (64 requests, one varlen launch); off by default so "
                          "that a kernel trace of the default run holds only the workload's attention launches")
@@ -58,12 +64,13 @@ def parse():
     return ap.parse_args()
 
 
-def profiled_figures(workload):
-    """Figures of the committed counter profile of this workload (HBM bytes
-    per attention launch, and where recorded the clock and MFMA-busy
-    fraction), if the kernel source is still the one that was profiled."""
+def profiled_figures(workload, mode="allgather"):
+    """Figures of the committed counter profile of this workload's launch in
+    this mode (HBM bytes per attention launch, and where recorded the clock
+    and MFMA-busy fraction), if the kernel source is still the one that was
+    profiled."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{mode}.txt")
     src = os.path.join(ROOT, "paper_2609_04774_amd", "csrc", "attn_partial.hip")
     if not os.path.exists(path):
         return None
@@ -75,7 +82,7 @@ def profiled_figures(workload):
             kv[key] = val
     with open(src, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
-    if kv.get("kernel_source_sha256") != sha:
+    if kv.get("kernel_source_sha256") != sha or kv.get("mode") != mode:
         return None
     out = {"traffic": int(kv["fetch_bytes"]) + int(kv["write_bytes"])}
     if "clock_ghz" in kv and "mfma_busy" in kv:
@@ -84,9 +91,9 @@ def profiled_figures(workload):
     return out
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, mode="allgather"):
     """HBM bytes per attention launch from the committed counter profile."""
-    f = profiled_figures(workload)
+    f = profiled_figures(workload, mode)
     return None if f is None else f["traffic"]
 
 
@@ -155,13 +162,14 @@ def heterogeneous_batch(args, gen, dev, stream, reps=5):
 def counter_profile(workload, args, rank):
     """The committed counter profile's clock and MFMA-busy fraction for this
     launch configuration (null when there is none for the current source)."""
-    if args.mode != "passkv" or rank != 0:
+    if rank != 0:
         return None
-    f = profiled_figures(workload)
+    f = profiled_figures(workload, args.mode)
     if f is None or "clock_ghz" not in f:
         return None
     return {"clock_ghz": f["clock_ghz"], "mfma_busy": f["mfma_busy"],
-            "source": f"profiles/traffic_{workload}.txt (rocprofv3 GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES)"}
+            "source": f"profiles/traffic_{workload}_{args.mode}.txt "
+                      "(rocprofv3 GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES)"}
 
 
 def main():
@@ -269,12 +277,9 @@ def main():
     merge_ms = sum(b.elapsed_time(c) for _, b, c in ev) / len(ev)
 
     rows_merged = n_rows * Hq
-    merge_bytes = (n_parts * rows_merged + rows_merged) * (4 * D + 4)
-    merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
     attn_tflops = flop / (attn_ms * 1e-3) / 1e12
     value = flop / (ms_step * 1e-3) / 1e12
 
-    # --- the KV-cache steps after the attention (not part of the timed step) --
     def timed(fn, reps=10):
         fn()
         torch.cuda.synchronize()
@@ -287,6 +292,30 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
 
+    # --- the merge ----------------------------------------------------------
+    # Algorithmic bytes: every partial's LSE, the O of each partial whose LSE
+    # is finite (a partial of weight 0 is not read), the merged O and LSE.
+    if args.mode == "passkv":
+        n_merged = n_parts
+        finite = int(torch.isfinite(l_parts).sum().item())
+        merge_what = (f"the step's merge of the {n_parts} pass-KV partials with restore "
+                      "(O of a partial with LSE = -inf is not read)")
+    else:
+        n_merged = C + (1 if P else 0)
+        m_o = torch.randn((n_merged, n_rows, Hq, D), generator=gen, device=dev)
+        m_l = 3.0 * torch.randn((n_merged, n_rows, Hq), generator=gen, device=dev)
+        m_out = torch.empty_like(out)
+        m_lse = torch.empty_like(out_lse)
+        merge_ms = timed(lambda: cp.attn_merge([m_o[i] for i in range(n_merged)], [m_l[i] for i in range(n_merged)],
+                                               m_out, m_lse, restore=plan, stream=stream))
+        finite = n_merged * rows_merged
+        merge_what = (f"{n_merged} partials of the rank's rows (seeded values, every LSE finite) "
+                      "merged with restore, as after pass-KV partials")
+        del m_o, m_l, m_out, m_lse
+    merge_bytes = finite * 4 * D + n_merged * rows_merged * 4 + rows_merged * (4 * D + 4)
+    merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
+
+    # --- the KV-cache steps after the attention (not part of the timed step) --
     # All C ranks of the request, as one GPU per rank would each do for its own.
     rank_rows = [torch.as_tensor(cp.shard_plan(P, R, C, r)[1] - P, device=dev) for r in range(C)]
     plans = [cp.shard_plan(P, R, C, r)[0] for r in range(C)]
@@ -364,14 +393,14 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(w.name) if args.mode == "passkv" and rank == 0 else None,
+            "traffic": measured_traffic(w.name, args.mode) if rank == 0 else None,
             "launch_ms": round(attn_ms, 4),
             "profiled": counter_profile(w.name, args, rank),
         },
         "merge": {
             "kernel": "lse_merge_kernel", "bound": "hbm", "ms": round(merge_ms, 4),
             "bytes": merge_bytes, "GB_s": round(merge_gbs, 1),
-            "frac": round(merge_gbs / PEAK_HBM_GBS, 4),
+            "frac": round(merge_gbs / PEAK_HBM_GBS, 4), "partials": n_merged, "what": merge_what,
         },
         "kv_writeback": {
             "kernel": "kv_writeback_kernel", "bound": "hbm", "ms": round(wb_ms, 4), "bytes": wb_bytes,

@@ -26,11 +26,21 @@ def test_traffic_figures_follow_the_kernel_source(tmp_path, monkeypatch):
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
     prof = tmp_path / "profiles"
     prof.mkdir()
-    (prof / "traffic_w.txt").write_text(f"# c\nkernel_source_sha256={sha}\nworkload=w\nfetch_bytes=10\nwrite_bytes=5\n")
-    (prof / "traffic_stale.txt").write_text("kernel_source_sha256=0\nworkload=stale\nfetch_bytes=10\nwrite_bytes=5\n")
+    (prof / "traffic_w_allgather.txt").write_text(
+        f"# c\nkernel_source_sha256={sha}\nworkload=w\nmode=allgather\nfetch_bytes=10\nwrite_bytes=5\n")
+    (prof / "traffic_w_passkv.txt").write_text(
+        f"kernel_source_sha256={sha}\nworkload=w\nmode=passkv\nfetch_bytes=20\nwrite_bytes=5\n")
+    (prof / "traffic_stale_allgather.txt").write_text(
+        "kernel_source_sha256=0\nworkload=stale\nmode=allgather\nfetch_bytes=10\nwrite_bytes=5\n")
+    # A file whose recorded mode is not the one its name says is not used.
+    (prof / "traffic_odd_passkv.txt").write_text(
+        f"kernel_source_sha256={sha}\nworkload=odd\nmode=allgather\nfetch_bytes=10\nwrite_bytes=5\n")
     (tmp_path / "paper_2609_04774_amd" / "csrc").mkdir(parents=True)
     (tmp_path / "paper_2609_04774_amd" / "csrc" / "attn_partial.hip").write_bytes(open(src, "rb").read())
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.measured_traffic("w") == 15
+    assert bench.measured_traffic("w", "allgather") == 15
+    assert bench.measured_traffic("w", "passkv") == 25
     assert bench.measured_traffic("stale") is None
+    assert bench.measured_traffic("odd", "passkv") is None
     assert bench.measured_traffic("missing") is None
