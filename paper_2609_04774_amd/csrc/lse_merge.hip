@@ -22,6 +22,7 @@ namespace {
 
 constexpr int kRowsPerGroup = 2;                      // rows merged by one 32-lane group
 constexpr int kRowsPerBlock = 8 * kRowsPerGroup;       // 256 threads = 8 groups
+constexpr int kPartsInFlight = 4;                      // partials whose O loads are issued together
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -78,17 +79,32 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeParams p) {
         if (i < p.n_parts) c[r][i] *= inv;
     }
   }
+  // Partials are taken kPartsInFlight at a time: all their O loads are
+  // issued before any is used, so a lane has up to kPartsInFlight x
+  // kRowsPerGroup 16-byte loads in flight.  The O of a partial of weight 0
+  // (LSE = -inf) is not read.
   f32x4 acc[kRowsPerGroup];
 #pragma unroll
   for (int r = 0; r < kRowsPerGroup; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < CP_MAX_MERGE_PARTS; ++i) {
-    if (i < p.n_parts) {
+  for (int i0 = 0; i0 < CP_MAX_MERGE_PARTS; i0 += kPartsInFlight) {
+    if (i0 < p.n_parts) {
+      f32x4 o[kPartsInFlight][kRowsPerGroup];
 #pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) {
-        if (c[r][i] != 0.f) {
-          const f32x4 o = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p.o[i] + (row0 + r) * kHeadDim) + lane);
-          acc[r] += c[r][i] * o;
+      for (int j = 0; j < kPartsInFlight; ++j) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerGroup; ++r) {
+          o[j][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (i0 + j < p.n_parts && c[r][i0 + j] != 0.f)
+            o[j][r] = __builtin_nontemporal_load(
+                reinterpret_cast<const f32x4*>(p.o[i0 + j] + (row0 + r) * kHeadDim) + lane);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kPartsInFlight; ++j) {
+        if (i0 + j < p.n_parts) {
+#pragma unroll
+          for (int r = 0; r < kRowsPerGroup; ++r) acc[r] += c[r][i0 + j] * o[j][r];
         }
       }
     }
