@@ -1,13 +1,16 @@
-"""GPU parity at the full workload sizes, in the launch configuration that
-bench.py times: one cp_attn_partial launch with the rank's C pass-KV partials
-(plus a prefix-only partial when a prefix is cached), then cp_attn_merge with
-the rank's plan, which writes every row to its place in the original order.
+"""GPU parity at the full workload sizes, in both launch configurations that
+bench.py times: its default step -- one cp_attn_partial launch of the rank's
+rows against every key they see in the all-gathered KV (and the paged
+prefix), then cp_attn_merge of that one partial with the rank's plan, which
+writes every row to its place in the original order -- and its --mode passkv
+step, one launch with the rank's C pass-KV partials (plus a prefix-only
+partial when a prefix is cached) merged and restored the same way.
 
 The oracle recomputes seeded samples of rows (every head) one by one: the
 first and last rows of each chunk, rows on both sides of 64- and 256-row
-boundaries, and random rows.  Properties that hold at any size are checked
-on every row: the merged pass-KV result equals the all-gathered partial, no
-NaN anywhere, and every restored row is written exactly once.
+boundaries, and random rows; both steps' rows are compared with it.
+Properties that hold at any size are checked on every row: the two steps
+agree, no NaN anywhere, and every restored row is written exactly once.
 """
 
 import numpy as np
@@ -37,7 +40,7 @@ def _inputs(w, rank):
 
 
 def _run_passkv(w, plan, q, k, v, pre):
-    """The bench's step: pass-KV partials (+ prefix partial) and the merge."""
+    """bench.py --mode passkv: pass-KV partials (+ prefix partial) and the merge."""
     n_parts = w.C + (1 if w.P else 0)
     o = torch.empty((n_parts, plan.n_rows, w.Hq, w.D), dtype=torch.float32, device=DEV)
     l = torch.empty((n_parts, plan.n_rows, w.Hq), dtype=torch.float32, device=DEV)
@@ -61,14 +64,19 @@ def _run_passkv(w, plan, q, k, v, pre):
 
 
 def _run_allgather(w, plan, q, k, v, pre):
+    """bench.py's default step: one partial over all visible keys, restored
+    by the merge of that one partial."""
     o = torch.empty((plan.n_rows, w.Hq, w.D), dtype=torch.float32, device=DEV)
     l = torch.empty((plan.n_rows, w.Hq), dtype=torch.float32, device=DEV)
     kc, vc, bt = (pre.k_cache, pre.v_cache, pre.block_table) if pre else (None, None, None)
     d = cp.make_desc(plan, q, k, v, o, l, kc, vc, bt, include_prefix=True, kv_rank=cp.CP_KV_ALL)
     ws = torch.empty(max(256, cp.workspace_size([d], w.Hq, w.Hkv)), dtype=torch.uint8, device=DEV)
     cp.attn_partial([d], w.Hq, w.Hkv, ws)
+    out = torch.full((w.R, w.Hq, w.D), float("nan"), dtype=torch.float32, device=DEV)
+    out_lse = torch.full((w.R, w.Hq), float("nan"), dtype=torch.float32, device=DEV)
+    cp.attn_merge([o], [l], out, out_lse, restore=plan)
     torch.cuda.synchronize()
-    return o, l
+    return out, out_lse
 
 
 def _sample_rows(plan, n_random, seed):
@@ -90,17 +98,18 @@ def _check_workload(name, rank, n_random):
     plan, rows, q, k, v, pre = _inputs(w, rank)
     ref_plan = oplan.shard_plan_fast(w.P, w.R, w.C, rank)
     assert rows.tolist() == ref_plan["row_pos"], "C-ABI plan differs from the oracle's"
+    out_ag, lse_ag = _run_allgather(w, plan, q, k, v, pre)
     out, out_lse = _run_passkv(w, plan, q, k, v, pre)
     # Every restored row of this rank is written, nothing else is.
     sel = torch.as_tensor(rows - w.P, device=DEV)
     written = torch.zeros(w.R, dtype=torch.bool, device=DEV)
     written[sel] = True
-    assert not torch.isnan(out[sel]).any() and not torch.isnan(out_lse[sel]).any()
-    assert torch.isnan(out_lse[~written]).all(), "merge wrote rows of another rank"
+    for o_, l_ in ((out_ag, lse_ag), (out, out_lse)):
+        assert not torch.isnan(o_[sel]).any() and not torch.isnan(l_[sel]).any()
+        assert torch.isnan(l_[~written]).all(), "merge wrote rows of another rank"
     # Merged pass-KV partials == the all-gathered partial, on every row.
-    o_ag, l_ag = _run_allgather(w, plan, q, k, v, pre)
-    assert float((o_ag - out[sel]).abs().max()) <= O_TOL
-    assert float((l_ag - out_lse[sel]).abs().max()) <= LSE_TOL
+    assert float((out_ag[sel] - out[sel]).abs().max()) <= O_TOL
+    assert float((lse_ag[sel] - out_lse[sel]).abs().max()) <= LSE_TOL
     # Sampled rows against the fp64 oracle.
     pick = _sample_rows(plan, n_random, w.seed)
     pos = rows[pick]
@@ -111,9 +120,9 @@ def _check_workload(name, rank, n_random):
         bt = pre.block_table.cpu().numpy().astype(np.int64)
     qq = f64(q[torch.as_tensor(pick, device=DEV)])
     O_ref, L_ref = oatt.rank_partial(qq, pos, w.P, kk, vv, kc, vc, bt)
-    got = out[torch.as_tensor(pos - w.P, device=DEV)]
-    got_l = out_lse[torch.as_tensor(pos - w.P, device=DEV)]
-    return compare(f64(got), f64(got_l), O_ref, L_ref, f"{name} rank {rank}")
+    at = torch.as_tensor(pos - w.P, device=DEV)
+    compare(f64(out_ag[at]), f64(lse_ag[at]), O_ref, L_ref, f"{name} rank {rank} all-gathered")
+    return compare(f64(out[at]), f64(out_lse[at]), O_ref, L_ref, f"{name} rank {rank} pass-KV")
 
 
 def test_llama3_8b_32k_rank0_full_size():
