@@ -102,7 +102,8 @@ typedef struct cp_rank_plan {
  *   out      host, required; filled on success.
  *   row_pos  host, optional (NULL): receives the global position of every
  *            local row, out->n_rows entries; row_pos_cap is its capacity.
- * Errors: CP_ERR_INVALID if C < 1, rank outside 0..C-1, P < 0, R < 0 or
+ * Errors: CP_ERR_INVALID if C < 1, rank outside 0..C-1, P < 0, R < 0,
+ * P > 2^31 or R > 2^31 (so that visible_pairs fits in 64 bits) or
  * out == NULL; CP_ERR_CAPACITY if row_pos != NULL and row_pos_cap < n_rows.
  * R = 0 and R < 2C are legal (empty chunks have q_len = 0).
  */

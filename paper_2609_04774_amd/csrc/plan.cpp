@@ -36,8 +36,9 @@ int make_plan(int64_t P, int64_t R, int32_t C, int32_t rank, cp_rank_plan* out) 
   if (C < 1) return fail(CP_ERR_INVALID, "cp_shard_plan: C must be >= 1");
   if (rank < 0 || rank >= C) return fail(CP_ERR_INVALID, "cp_shard_plan: rank outside 0..C-1");
   if (P < 0 || R < 0) return fail(CP_ERR_INVALID, "cp_shard_plan: negative prefix or suffix length");
-  if (R > ((int64_t)1 << 40) || P > ((int64_t)1 << 40))
-    return fail(CP_ERR_INVALID, "cp_shard_plan: length beyond 2^40 tokens");
+  // P, R <= 2^31 keeps visible_pairs (< R P + R^2) below 2^63.
+  if (R > ((int64_t)1 << 31) || P > ((int64_t)1 << 31))
+    return fail(CP_ERR_INVALID, "cp_shard_plan: prefix or suffix beyond 2^31 tokens");
   const int64_t two_c = 2 * (int64_t)C;
   const int64_t s = (R + two_c - 1) / two_c;
   cp_rank_plan p;

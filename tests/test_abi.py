@@ -108,6 +108,23 @@ def test_plan_errors():
     assert cp.last_error() == ""
 
 
+def test_plan_length_limit_keeps_visible_pairs_exact():
+    """Up to 2^31 cached and 2^31 new tokens the pair count W(R, P) =
+    RP + R(R+1)/2 (Sec. 2.2) is exact in 64 bits; longer inputs are refused
+    rather than wrapped."""
+    plan = cp.CpRankPlan()
+    big = 1 << 31
+    assert cp.lib.cp_shard_plan(big + 1, 10, 2, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(0, big + 1, 2, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+    assert cp.lib.cp_shard_plan(big, big, 1, 0, ctypes.byref(plan), None, 0) == cp.CP_OK
+    assert plan.visible_pairs == big * big + big * (big + 1) // 2
+    total = 0
+    for r in range(4):
+        assert cp.lib.cp_shard_plan(big, big, 4, r, ctypes.byref(plan), None, 0) == cp.CP_OK
+        total += plan.visible_pairs
+    assert total == big * big + big * (big + 1) // 2
+
+
 FAKE = 1 << 20          # aligned addresses that are never dereferenced
 
 
