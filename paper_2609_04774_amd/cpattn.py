@@ -165,9 +165,51 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _dev(t, name: str, dtype=None, rows: Optional[int] = None, tail=None):
+    """Checks that a tensor argument is what the C ABI will read or write
+    through its pointer: a contiguous GPU tensor of the right element type,
+    with at least ``rows`` entries along its first dimension and, if given,
+    trailing dimensions ``tail``.  The library sees only the pointer, so a
+    tensor that is too small or of another type would be read or written out
+    of bounds; these checks turn that into an exception."""
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if rows is not None and (t.dim() == 0 or t.shape[0] < rows):
+        raise ValueError(f"{name} needs at least {rows} rows, has shape {tuple(t.shape)}")
+    if tail is not None and tuple(t.shape[1:]) != tuple(tail):
+        raise ValueError(f"{name} must have shape [*, {', '.join(map(str, tail))}], has {tuple(t.shape)}")
+
+
 def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=None,
               block_table=None, include_prefix: bool = True, kv_rank: int = CP_KV_ALL) -> CpPartialDesc:
-    """A cp_partial_desc over torch device tensors (layouts in include/cp_attn.h)."""
+    """A cp_partial_desc over torch device tensors (layouts in include/cp_attn.h).
+    The tensors' head counts are checked against n_heads_q / n_heads_kv when
+    the descriptor is launched."""
+    import torch
+    D = CP_HEAD_DIM
+    _dev(q, "q", torch.bfloat16, plan.n_rows)
+    _dev(o, "o", torch.float32, plan.n_rows)
+    _dev(lse, "lse", torch.float32, plan.n_rows)
+    _dev(k_new, "k_new", torch.bfloat16, plan.new_len)
+    _dev(v_new, "v_new", torch.bfloat16, plan.new_len)
+    _dev(k_cache, "k_cache", torch.bfloat16)
+    _dev(v_cache, "v_cache", torch.bfloat16)
+    _dev(block_table, "block_table", torch.int32)
+    if include_prefix and plan.prefix_len > 0 and block_table is not None:
+        if block_table.numel() < -(-plan.prefix_len // CP_KV_BLOCK_TOKENS):
+            raise ValueError("block_table shorter than ceil(P / 16)")
+    for name, t in (("q", q), ("o", o), ("k_new", k_new), ("v_new", v_new)):
+        if t is not None and (t.dim() != 3 or t.shape[2] != D):
+            raise ValueError(f"{name} must have shape [rows, heads, {D}], has {tuple(t.shape)}")
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+        if t is not None and (t.dim() != 4 or t.shape[1] != CP_KV_BLOCK_TOKENS or t.shape[3] != D):
+            raise ValueError(f"{name} must have shape [blocks, 16, heads, {D}], has {tuple(t.shape)}")
     d = CpPartialDesc()
     d.plan = plan
     d.q = _ptr(q)
@@ -180,7 +222,25 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
     d.kv_rank = kv_rank
     d.o = _ptr(o)
     d.lse = _ptr(lse)
+    d._heads = (q, o, lse, k_new, v_new, k_cache, v_cache)
     return d
+
+
+def _check_heads(descs, n_heads_q: int, n_heads_kv: int):
+    for i, d in enumerate(descs):
+        held = getattr(d, "_heads", None)
+        if held is None:
+            continue
+        q, o, lse, k_new, v_new, k_cache, v_cache = held
+        for name, t, h in (("q", q, n_heads_q), ("o", o, n_heads_q), ("k_new", k_new, n_heads_kv),
+                           ("v_new", v_new, n_heads_kv)):
+            if t is not None and t.shape[1] != h:
+                raise ValueError(f"desc {i}: {name} has {t.shape[1]} heads, expected {h}")
+        if lse is not None and (lse.dim() != 2 or lse.shape[1] != n_heads_q):
+            raise ValueError(f"desc {i}: lse must have shape [rows, {n_heads_q}], has {tuple(lse.shape)}")
+        for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+            if t is not None and t.shape[2] != n_heads_kv:
+                raise ValueError(f"desc {i}: {name} has {t.shape[2]} heads, expected {n_heads_kv}")
 
 
 def _desc_array(descs: Sequence[CpPartialDesc]):
@@ -213,6 +273,8 @@ def attn_partial(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int
     ``workspace`` is a torch uint8 device tensor of at least
     ``workspace_size(descs, ...)`` bytes.
     """
+    _check_heads(descs, n_heads_q, n_heads_kv)
+    _dev(workspace, "workspace")
     arr = _desc_array(descs)
     nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
     _check(lib.cp_attn_partial(arr, len(descs), n_heads_q, n_heads_kv, head_dim,
@@ -226,6 +288,22 @@ def attn_merge(o_parts, lse_parts, o_out, lse_out=None, restore: Optional[CpRank
     """cp_attn_merge of torch device tensors; bf16 output when o_out is bf16."""
     import torch
     n = len(o_parts)
+    if len(lse_parts) != n:
+        raise ValueError("o_parts and lse_parts differ in length")
+    rows = o_parts[0].shape[0] if n_tokens is None else n_tokens
+    heads = o_parts[0].shape[1] if n_heads is None else n_heads
+    for i in range(n):
+        _dev(o_parts[i], f"o_parts[{i}]", torch.float32, rows)
+        _dev(lse_parts[i], f"lse_parts[{i}]", torch.float32, rows)
+        if o_parts[i].numel() < rows * heads * head_dim or lse_parts[i].numel() < rows * heads:
+            raise ValueError(f"partial {i} holds fewer than {rows} x {heads} rows")
+    out_rows = restore.new_len if restore is not None else rows
+    _dev(o_out, "o_out", None, out_rows)
+    if o_out.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("o_out must be float32 or bfloat16")
+    _dev(lse_out, "lse_out", torch.float32, out_rows)
+    if o_out.numel() < out_rows * heads * head_dim or (lse_out is not None and lse_out.numel() < out_rows * heads):
+        raise ValueError(f"outputs hold fewer than {out_rows} x {heads} rows")
     optrs = (ctypes.c_void_p * max(1, n))(*[_ptr(o) for o in o_parts])
     lptrs = (ctypes.c_void_p * max(1, n))(*[_ptr(s) for s in lse_parts])
     if n_tokens is None:
@@ -245,7 +323,15 @@ def default_scale(head_dim: int = CP_HEAD_DIM) -> float:
 def kv_writeback(plan: CpRankPlan, k_rows, v_rows, k_cache, v_cache, block_table, stream=None):
     """cp_kv_writeback of torch device tensors: the rank's rows [n_rows, Hkv, D]
     (plan order) into caches [n_blocks, 16, Hkv, D] through block_table."""
+    import torch
     n_blocks, _, Hkv, D = k_cache.shape
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, name, torch.bfloat16, None, (CP_KV_BLOCK_TOKENS, Hkv, D))
+    if v_cache.shape[0] != n_blocks:
+        raise ValueError("k_cache and v_cache differ in blocks")
+    _dev(k_rows, "k_rows", torch.bfloat16, plan.n_rows, (Hkv, D))
+    _dev(v_rows, "v_rows", torch.bfloat16, plan.n_rows, (Hkv, D))
+    _dev(block_table, "block_table", torch.int32)
     _check(lib.cp_kv_writeback(ctypes.byref(plan), _ptr(k_rows), _ptr(v_rows), Hkv, D, _ptr(k_cache),
                                _ptr(v_cache), n_blocks, _ptr(block_table), block_table.numel(),
                                _stream_handle(stream)))
@@ -255,7 +341,15 @@ def kv_gather(k_cache, v_cache, block_table, pos_begin: int, k_rows, v_rows, str
     """cp_kv_gather of torch device tensors: positions pos_begin ..
     pos_begin + len(k_rows) - 1 out of caches [n_blocks, 16, Hkv, D] through
     block_table into k_rows, v_rows [n, Hkv, D]."""
+    import torch
     n_blocks, _, Hkv, D = k_cache.shape
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, name, torch.bfloat16, None, (CP_KV_BLOCK_TOKENS, Hkv, D))
+    if v_cache.shape[0] != n_blocks:
+        raise ValueError("k_cache and v_cache differ in blocks")
+    _dev(k_rows, "k_rows", torch.bfloat16, None, (Hkv, D))
+    _dev(v_rows, "v_rows", torch.bfloat16, k_rows.shape[0], (Hkv, D))
+    _dev(block_table, "block_table", torch.int32)
     _check(lib.cp_kv_gather(_ptr(k_cache), _ptr(v_cache), n_blocks, _ptr(block_table), block_table.numel(),
                             pos_begin, k_rows.shape[0], Hkv, D, _ptr(k_rows), _ptr(v_rows),
                             _stream_handle(stream)))
@@ -266,6 +360,11 @@ def repartition(prefix_len: int, new_len: int, src_rows, C_dst: int, dst_rank: i
     ranks' row tensors (plan order); dst_rows receives rank dst_rank's rows at
     degree C_dst.  A row is everything after a tensor's first dimension."""
     C_src = len(src_rows)
+    dst_plan, _ = shard_plan(prefix_len, new_len, C_dst, dst_rank, with_rows=False)
+    _dev(dst_rows, "dst_rows", None, dst_plan.n_rows)
+    for r, t in enumerate(src_rows):
+        src_plan, _ = shard_plan(prefix_len, new_len, C_src, r, with_rows=False)
+        _dev(t, f"src_rows[{r}]", dst_rows.dtype, src_plan.n_rows, tuple(dst_rows.shape[1:]))
     ptrs = (ctypes.c_void_p * max(1, C_src))(*[_ptr(t) if t.numel() else None for t in src_rows])
     row_bytes = math.prod(dst_rows.shape[1:]) * dst_rows.element_size()
     _check(lib.cp_repartition(prefix_len, new_len, C_src, ptrs, C_dst, dst_rank, _ptr(dst_rows), row_bytes,

@@ -317,3 +317,13 @@ def test_repartition_argument_errors():
     assert _rp_status(P=-1) == cp.CP_ERR_INVALID
     assert _rp_status(P=1 << 31, R=64) == cp.CP_ERR_UNSUPPORTED
     assert cp.last_error() != ""
+
+
+def test_binding_refuses_host_tensors():
+    """The binding checks a tensor argument before taking its pointer: host
+    memory is refused (the kernels would dereference it on the GPU)."""
+    import torch
+    plan, _ = cp.shard_plan(0, 64, 2, 0)
+    q = torch.zeros((plan.n_rows, 8, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        cp.make_desc(plan, q, None, None, None, None, include_prefix=False, kv_rank=cp.CP_KV_NONE)

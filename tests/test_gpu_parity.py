@@ -189,7 +189,8 @@ def test_empty_and_degenerate_launches():
     # R = 0: every rank is empty; the call is a no-op.
     plan, _ = cp.shard_plan(0, 0, 2, 0)
     o, lse = gc.alloc_out(1, 8)
-    desc = cp.make_desc(plan, o, None, None, o, lse)
+    q = torch.zeros((1, 8, 128), dtype=torch.bfloat16, device=o.device)
+    desc = cp.make_desc(plan, q, None, None, o, lse)
     gc.run_partials([desc], 8, 2)
     assert torch.isnan(o).all()
     # One token: it sees exactly itself, so O = v_0 and LSE = q.k/sqrt(D).
