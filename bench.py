@@ -134,7 +134,7 @@ def heterogeneous_batch(args, gen, dev, stream, reps=5):
             o = torch.empty((plan.n_rows, Hq, D), dtype=torch.float32, device=dev)
             lse = torch.empty((plan.n_rows, Hq), dtype=torch.float32, device=dev)
             descs.append(cp.make_desc(plan, q, k, v, o, lse, k_pool, v_pool, table, include_prefix=True))
-            keep.append((q, k, v, o, lse))
+            keep.append((q, k, v, o, lse, table))
             pairs += plan.visible_pairs
     ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=dev)
     for _ in range(2):

@@ -190,7 +190,8 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
               block_table=None, include_prefix: bool = True, kv_rank: int = CP_KV_ALL) -> CpPartialDesc:
     """A cp_partial_desc over torch device tensors (layouts in include/cp_attn.h).
     The tensors' head counts are checked against n_heads_q / n_heads_kv when
-    the descriptor is launched."""
+    the descriptor is launched.  The descriptor keeps references to its
+    tensors; keep it until the launch has been issued."""
     import torch
     D = CP_HEAD_DIM
     _dev(q, "q", torch.bfloat16, plan.n_rows)
@@ -223,6 +224,11 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
     d.o = _ptr(o)
     d.lse = _ptr(lse)
     d._heads = (q, o, lse, k_new, v_new, k_cache, v_cache)
+    # The descriptor holds only device pointers: keep every tensor it points
+    # at alive for as long as the descriptor exists, so that a caller that
+    # drops its own reference (say to a block table built per request) before
+    # the launch cannot leave the kernel reading freed, reused memory.
+    d._keep = (q, k_new, v_new, k_cache, v_cache, block_table, o, lse)
     return d
 
 

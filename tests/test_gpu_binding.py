@@ -58,3 +58,24 @@ def test_merge_and_cache_checks():
         cp.kv_gather(kc, vc, table.long(), 0, _bf(16, 2, 128), _bf(16, 2, 128))
     with pytest.raises(ValueError):
         cp.repartition(0, 64, [rows, rows[:1]], 4, 0, _bf(16, 2, 128))  # a source rank too small
+
+
+def test_descriptor_keeps_its_tensors_alive():
+    """A block table (or any other tensor) handed to make_desc stays allocated
+    while the descriptor exists, even when the caller drops its own
+    reference: its memory cannot be reused before the launch reads it."""
+    import gc
+    import weakref
+    plan, _ = cp.shard_plan(64, 64, 2, 0)
+    q, k, v = _bf(plan.n_rows, 8, 128), _bf(64, 2, 128), _bf(64, 2, 128)
+    o, lse = _f32(plan.n_rows, 8, 128), _f32(plan.n_rows, 8)
+    kc, vc = _bf(4, 16, 2, 128), _bf(4, 16, 2, 128)
+    table = torch.arange(4, dtype=torch.int32, device=DEV)
+    ref = weakref.ref(table)
+    d = cp.make_desc(plan, q, k, v, o, lse, kc, vc, table, include_prefix=True)
+    del table
+    gc.collect()
+    assert ref() is not None and ref().data_ptr() == d.block_table
+    del d
+    gc.collect()
+    assert ref() is None
