@@ -132,10 +132,19 @@ def gather_paged(cache, block_table, length, block_tokens=BLOCK_TOKENS):
 
     cache: [n_blocks, block_tokens, Hkv, D]; logical token j lives in physical
     block block_table[j // block_tokens], slot j % block_tokens.
+
+    Reading (the paper says nothing of invalid entries): an entry outside
+    [0, n_blocks) names no block of the cache, so nothing is read through it
+    and the rows of its tokens are zeros -- in attention, keys of logit 0 and
+    values 0.
     """
     cache = _f64(cache)
     table = np.asarray(block_table, dtype=np.int64)
-    rows = [cache[table[j // block_tokens], j % block_tokens] for j in range(length)]
+    zero = np.zeros(cache.shape[2:], dtype=np.float64)
+    rows = []
+    for j in range(length):
+        blk = table[j // block_tokens]
+        rows.append(cache[blk, j % block_tokens] if 0 <= blk < cache.shape[0] else zero)
     if not rows:
         return np.zeros((0,) + cache.shape[2:], dtype=np.float64)
     return np.stack(rows)

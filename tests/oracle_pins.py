@@ -188,6 +188,33 @@ def check_paged_prefix(full_causal_attention, rank_partial, gather_paged, seed=5
         O_p, L_p = rank_partial(q[P:], rows, P, k[P:], v[P:], k_cache, v_cache, table)
         assert np.max(np.abs(O_p - O_full[P:])) <= 1e-12, "prefix + suffix != recompute"
         assert np.max(np.abs(L_p - L_full[P:])) <= 1e-12, "prefix + suffix LSE != recompute"
+    # Entries outside the cache read as zero rows: addressing by hand, then
+    # attention through such a table == recomputation with those prefix rows
+    # zeroed (keys of logit 0, values 0).
+    cache = np.arange(3 * B, dtype=np.float64).reshape(3, B, 1, 1)
+    got = gather_paged(cache, [1, -1, 3, 0], 4 * B).reshape(-1)
+    assert got[:B].tolist() == list(range(B, 2 * B)), "valid entry before bad ones"
+    assert not got[B:3 * B].any(), "entries -1 and n_blocks must read as zeros"
+    assert got[3 * B:].tolist() == list(range(B)), "valid entry after bad ones"
+    P, R = 64, 24
+    q = rng.standard_normal((P + R, Hq, D)) * 2.0
+    k = rng.standard_normal((P + R, Hkv, D))
+    v = rng.standard_normal((P + R, Hkv, D))
+    table = np.array([2, -1, 0, 7])              # 4 cache blocks: entry 7 is past the end
+    k_cache = rng.standard_normal((4, B, Hkv, D))
+    v_cache = rng.standard_normal((4, B, Hkv, D))
+    kz, vz = k.copy(), v.copy()
+    for b, blk in enumerate(table):
+        if 0 <= blk < 4:
+            k_cache[blk] = k[b * B:(b + 1) * B]
+            v_cache[blk] = v[b * B:(b + 1) * B]
+        else:
+            kz[b * B:(b + 1) * B] = 0.0
+            vz[b * B:(b + 1) * B] = 0.0
+    O_full, L_full = full_causal_attention(q, kz, vz)
+    O_p, L_p = rank_partial(q[P:], np.arange(P, P + R), P, k[P:], v[P:], k_cache, v_cache, table)
+    assert np.max(np.abs(O_p - O_full[P:])) <= 1e-12, "bad entries are not zero keys and values"
+    assert np.max(np.abs(L_p - L_full[P:])) <= 1e-12, "bad entries: LSE"
 
 
 def check_plan(shard_plan, remaining_workload, shard_plan_fast=None):
@@ -213,6 +240,57 @@ def check_plan(shard_plan, remaining_workload, shard_plan_fast=None):
                 assert shard_plan_fast(P, R, C, r) == plan
         assert total == remaining_workload(R, P), "sum over ranks != W(R, P)"
         assert sorted(seen) == list(range(P, P + R)), "rows are not a bijection onto the suffix"
+
+
+GOLDEN_DIR = __import__("os").path.join(__import__("os").path.dirname(__import__("os").path.abspath(__file__)),
+                                        "golden")
+
+
+def _golden_passkv_shards():
+    rows = []
+    with open(GOLDEN_DIR + "/passkv_shards.txt") as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            P, R, C, s, ids, ranges = line.split()
+            rng = [] if ranges == "-" else [tuple(int(x) for x in r.split("-")) for r in ranges.split(",")]
+            rows.append((int(P), int(R), int(C), int(s), tuple(int(x) for x in ids.split(",")), rng))
+    return rows
+
+
+def check_kv_shards(kv_shard_ranges, shard_plan):
+    """Pass-KV shard s is the suffix K/V rank s holds under the zigzag split
+    (Sec. 2.1): its chunks s and 2C-1-s.  Checked against ranges worked by hand
+    (tests/golden/passkv_shards.txt), and against the pinned plan: shard s's
+    ranges are exactly the contiguous runs of rank s's row positions, and the C
+    shards partition the suffix."""
+    cases = _golden_passkv_shards()
+    assert len(cases) >= 18
+    for P, R, C, s, ids, want in cases:
+        assert [tuple(r) for r in kv_shard_ranges(P, R, C, s)] == want, (P, R, C, s)
+        assert ids == (s, 2 * C - 1 - s)
+    for P, R, C in [(0, 1024, 2), (0, 70, 4), (16, 37, 8), (32, 5, 4), (0, 64, 1), (48, 3, 2), (16, 37, 3),
+                    (0, 1000, 8)]:
+        keys = []
+        for s in range(C):
+            pos = shard_plan(P, R, C, s)["row_pos"]
+            runs = []
+            for p in pos:
+                if runs and runs[-1][1] == p:
+                    runs[-1][1] = p + 1
+                else:
+                    runs.append([p, p + 1])
+            got = [tuple(r) for r in kv_shard_ranges(P, R, C, s)]
+            merged = []
+            for lo, hi in got:                      # two adjacent chunks form one run
+                if merged and merged[-1][1] == lo:
+                    merged[-1] = (merged[-1][0], hi)
+                else:
+                    merged.append((lo, hi))
+            assert merged == [tuple(r) for r in runs], (P, R, C, s)
+            for lo, hi in got:
+                keys.extend(range(lo, hi))
+        assert sorted(keys) == list(range(P, P + R)), "shards do not partition the suffix"
 
 
 def check_read_paged(read_paged, write_paged, seed=12):

@@ -79,6 +79,10 @@ def test_inverse_map_is_the_inverse():
             assert plan["row_pos"][row_of[i]] == P + i
 
 
+def test_kv_shards_match_hand_worked_zigzag_shards():
+    pins.check_kv_shards(oplan.kv_shard_ranges, oplan.shard_plan_fast)
+
+
 def test_kv_shards_partition_the_suffix():
     for P, R, C in [(0, 1024, 2), (32, 37, 8), (0, 3, 4)]:
         covered = []

@@ -41,6 +41,7 @@ def _all_pins(att, plan, cache=None):
         lambda: pins.check_merge(att.full_causal_attention, att.attend, att.lse_merge),
         lambda: pins.check_paged_prefix(att.full_causal_attention, att.rank_partial, att.gather_paged),
         lambda: pins.check_plan(plan.shard_plan, plan.remaining_workload, plan.shard_plan_fast),
+        lambda: pins.check_kv_shards(plan.kv_shard_ranges, plan.shard_plan_fast),
     ]
     failed = 0
     for c in checks:
@@ -60,7 +61,10 @@ ATTENTION_MUTATIONS = [
     ("output not normalised", "out_rows = (e @ vg) / denom[:, None]", "out_rows = (e @ vg)"),
     ("merge weight sign", "np.exp(stack - safe_mx)", "np.exp(safe_mx - stack)"),
     ("merge ignores the max", "lse = np.where(live, safe_mx + np.log(", "lse = np.where(live, 0 * safe_mx + np.log("),
-    ("block table ignored", "cache[table[j // block_tokens], j % block_tokens]", "cache[j // block_tokens, j % block_tokens]"),
+    ("block table ignored", "rows.append(cache[blk, j % block_tokens] if", "rows.append(cache[j // block_tokens, j % block_tokens] if"),
+    ("gather of a bad entry wraps", "if 0 <= blk < cache.shape[0] else zero)", "if blk < cache.shape[0] else zero)"),
+    ("gather of a bad entry is skipped", "if 0 <= blk < cache.shape[0] else zero)",
+     "if 0 <= blk < cache.shape[0] else cache[0, 0])"),
     ("suffix off by one", "suffix_ranges = [(P, P + R)]", "suffix_ranges = [(P + 1, P + R)]"),
     ("suffix keys at wrong positions", "ps.append(np.arange(P + lo_i, P + hi_i, dtype=np.int64))",
      "ps.append(np.arange(lo_i, hi_i, dtype=np.int64))"),
@@ -72,6 +76,12 @@ PLAN_MUTATIONS = [
     ("no padding", "padded = -(-R // (2 * C)) * (2 * C)", "padded = R"),
     ("W drops the prefix term", "return R * P + R * (R + 1) // 2", "return R * (R + 1) // 2"),
     ("diagonal not counted", "for _key in range(pos + 1):", "for _key in range(pos):"),
+    ("pass-KV shard holds chunks s and C+s", "for chunk_id in (shard, 2 * C - 1 - shard):",
+     "for chunk_id in (shard, C + shard):"),
+    ("pass-KV shard holds its first chunk only", "for chunk_id in (shard, 2 * C - 1 - shard):",
+     "for chunk_id in (shard,):"),
+    ("pass-KV shard keeps padding keys", "        hi = min(R, lo + s)\n        if hi > lo:\n            out.append((P + lo, P + hi))",
+     "        hi = lo + s\n        if hi > lo:\n            out.append((P + lo, P + hi))"),
 ]
 
 
