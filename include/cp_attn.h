@@ -37,9 +37,12 @@
  *     null stream) and return after host-side validation and the launch.
  *   - Errors: every call returns CP_OK (0) or a negative status, checks its
  *     arguments before launching anything, and launches nothing on error.
+ *     No call throws: a host-side failure inside the library (exhausted
+ *     host memory) is returned as CP_ERR_HOST.
  *     cp_last_error() gives a readable reason for the calling thread's last
- *     failure.  Device-side contents (e.g. a block-table entry outside the
- *     cache) are not checked: out-of-range entries are undefined behaviour.
+ *     failure.  Block-table entries outside the cache are handled on the
+ *     device as each call states (never read or written through); other
+ *     device-side contents are not checked.
  */
 #ifndef CP_ATTN_H_
 #define CP_ATTN_H_
@@ -56,20 +59,23 @@ extern "C" {
 #define CP_ERR_UNSUPPORTED (-2) /* well-formed but not built for (e.g. D != 128) */
 #define CP_ERR_HIP (-3)         /* the HIP runtime reported an error */
 #define CP_ERR_CAPACITY (-4)    /* a caller buffer is too small */
+#define CP_ERR_HOST (-5)        /* host-side failure: out of host memory or an internal error */
 
 #define CP_HEAD_DIM 128
 #define CP_KV_BLOCK_TOKENS 16
 #define CP_MAX_MERGE_PARTS 16
-#define CP_MAX_DEGREE 64        /* largest C of cp_repartition */
+#define CP_MAX_DEGREE 64        /* largest CP degree C of any call */
 
 /* kv_rank values of cp_partial_desc besides a rank number 0..C-1. */
 #define CP_KV_ALL (-1)  /* every causally visible suffix key (all-gathered KV) */
 #define CP_KV_NONE (-2) /* no suffix key (prefix-only partial) */
 
-/* Static description of a status code. */
+/* Static description of a status code.  (Library utility; not from the
+ * paper.) */
 const char* cp_status_string(int status);
 
-/* Detail of the calling thread's most recent failing call ("" if none). */
+/* Detail of the calling thread's most recent failing call ("" if none).
+ * (Library utility; not from the paper.) */
 const char* cp_last_error(void);
 
 /* ---------------------------------------------------------------------- */
@@ -102,9 +108,10 @@ typedef struct cp_rank_plan {
  *   out      host, required; filled on success.
  *   row_pos  host, optional (NULL): receives the global position of every
  *            local row, out->n_rows entries; row_pos_cap is its capacity.
- * Errors: CP_ERR_INVALID if C < 1, rank outside 0..C-1, P < 0, R < 0,
- * P > 2^31 or R > 2^31 (so that visible_pairs fits in 64 bits) or
- * out == NULL; CP_ERR_CAPACITY if row_pos != NULL and row_pos_cap < n_rows.
+ * Errors: CP_ERR_INVALID if C < 1, C > CP_MAX_DEGREE, rank outside
+ * 0..C-1, P < 0, R < 0, P > 2^31 or R > 2^31 (so that visible_pairs fits in
+ * 64 bits) or out == NULL; CP_ERR_CAPACITY if row_pos != NULL and
+ * row_pos_cap < n_rows.
  * R = 0 and R < 2C are legal (empty chunks have q_len = 0).
  */
 int cp_shard_plan(int64_t prefix_len, int64_t new_len, int32_t C, int32_t rank,
@@ -114,7 +121,8 @@ int cp_shard_plan(int64_t prefix_len, int64_t new_len, int32_t C, int32_t rank,
  * Restore map (Sec. 2.1): for each suffix index i in 0..R-1, the rank that
  * holds it and its local row there.  rank_of (int32) and row_of (int64) are
  * host arrays of capacity `cap` >= R.
- * Errors: CP_ERR_INVALID for bad P/R/C or NULL arrays; CP_ERR_CAPACITY if cap < R.
+ * Errors: CP_ERR_INVALID for bad P/R/C (as cp_shard_plan) or NULL arrays;
+ * CP_ERR_CAPACITY if cap < R.
  */
 int cp_shard_inverse(int64_t prefix_len, int64_t new_len, int32_t C,
                      int32_t* rank_of, int64_t* row_of, int64_t cap);
@@ -134,7 +142,10 @@ int cp_shard_inverse(int64_t prefix_len, int64_t new_len, int32_t C,
  *   k_cache,v_cache  bf16 [n_blocks][16][Hkv][D]: paged prefix cache.
  *   block_table int32 [P/16]: physical block of each logical prefix block.
  *               The three prefix pointers may be NULL unless include_prefix
- *               and P > 0; then P must be a multiple of 16.
+ *               and P > 0; then P must be a multiple of 16.  An entry
+ *               outside [0, n_blocks) names no block of the cache: its 16
+ *               tokens' keys and values read as zeros (nothing is read
+ *               through it), as in cp_kv_gather.
  *   include_prefix  1: rows attend to all P prefix keys; 0: to none.
  *   kv_rank     CP_KV_ALL: rows attend to every suffix key at or before them
  *               (the paper's all-gathered CP); r in 0..C-1: only to the suffix
@@ -142,6 +153,8 @@ int cp_shard_inverse(int64_t prefix_len, int64_t new_len, int32_t C,
  *               shards partition the suffix); CP_KV_NONE: to no suffix key.
  *   o           fp32 [plan.n_rows][Hq][D], normalised partial output.
  *   lse         fp32 [plan.n_rows][Hq], natural-log LSE (-inf: no key).
+ *   n_blocks    blocks in k_cache and v_cache; >= 1 when the prefix is read.
+ *               Values above 2^31 - 1 act as 2^31 - 1 (entries are int32).
  * Merging (cp_attn_merge) the C pass-KV partials plus a prefix-only partial
  * gives the CP_KV_ALL result with include_prefix = 1.
  */
@@ -157,9 +170,12 @@ typedef struct cp_partial_desc {
   int32_t kv_rank;
   float* o;
   float* lse;
+  int64_t n_blocks;
 } cp_partial_desc;
 
 /*
+ * Sizing call of cp_attn_partial (Sec. 2.1, 2.2 partial attention; the
+ * workspace itself is a library interface, not from the paper).
  * Device workspace bytes cp_attn_partial needs for this descriptor set: the
  * device copy of the descriptors and the scheduled work list, and, when the
  * set has few work items with long key walks (a short suffix over a long
@@ -172,9 +188,11 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
                                       int32_t n_heads_q, int32_t n_heads_kv);
 
 /*
- * Partial attention of every descriptor, in one kernel launch (plus, when
- * key walks were split, one launch that merges each walk's pieces exactly,
- * by the log-sum-exp combination of paper Sec. 2.1).
+ * Partial attention of every descriptor (Sec. 2.1: each rank's local queries
+ * against the causally visible keys; Sec. 2.2: the cached prefix's keys
+ * included), in one kernel launch, plus, when key walks were split, one
+ * launch that combines each walk's pieces with the log-sum-exp identity
+ * cp_attn_merge applies (exact: the pieces cover disjoint key sets).
  *   descs       host array of n_descs descriptors (read during the call only);
  *               n_descs == 0 is a no-op.  Descriptors may come from different
  *               requests (ragged lengths); output buffers must not overlap.
@@ -205,6 +223,13 @@ int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_hea
  * Merge n_parts partials of the same rows that were computed over disjoint
  * key sets:  LSE = ln sum_i e^{LSE_i},  O = sum_i e^{LSE_i - LSE} O_i
  * (partials with LSE_i = -inf weigh 0; all -inf gives O = 0, LSE = -inf).
+ * Source: the paper defines no partial outputs.  This is the exact identity
+ * for a softmax over a union of disjoint key sets (the online-softmax
+ * recurrence of Milakov & Gimelshein, 2018), which the ring-attention CP
+ * scheme Sec. 2.1 cites as an alternative (Liu et al., 2024) needs to combine
+ * the partials of successive KV shards.  With one partial and a restore plan
+ * it is Sec. 2.1's final step alone: the rank's outputs put back in sequence
+ * order, which concatenated over the ranks equals single-rank attention.
  *   o_parts, lse_parts  host arrays of n_parts device pointers (1..16):
  *               o_parts[i] fp32 [n_tokens][n_heads][D], lse_parts[i] fp32
  *               [n_tokens][n_heads].  n_parts == 1 copies (and restores).

@@ -21,6 +21,7 @@ CP_ERR_INVALID = -1
 CP_ERR_UNSUPPORTED = -2
 CP_ERR_HIP = -3
 CP_ERR_CAPACITY = -4
+CP_ERR_HOST = -5
 CP_HEAD_DIM = 128
 CP_KV_BLOCK_TOKENS = 16
 CP_MAX_MERGE_PARTS = 16
@@ -62,7 +63,8 @@ class CpPartialDesc(ctypes.Structure):
                 ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
                 ("block_table", ctypes.c_void_p),
                 ("include_prefix", ctypes.c_int32), ("kv_rank", ctypes.c_int32),
-                ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
+                ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p),
+                ("n_blocks", ctypes.c_int64)]
 
 
 class CpError(RuntimeError):
@@ -211,6 +213,8 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
     for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
         if t is not None and (t.dim() != 4 or t.shape[1] != CP_KV_BLOCK_TOKENS or t.shape[3] != D):
             raise ValueError(f"{name} must have shape [blocks, 16, heads, {D}], has {tuple(t.shape)}")
+    if k_cache is not None and v_cache is not None and k_cache.shape[0] != v_cache.shape[0]:
+        raise ValueError("k_cache and v_cache differ in blocks")
     d = CpPartialDesc()
     d.plan = plan
     d.q = _ptr(q)
@@ -223,6 +227,7 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
     d.kv_rank = kv_rank
     d.o = _ptr(o)
     d.lse = _ptr(lse)
+    d.n_blocks = k_cache.shape[0] if k_cache is not None else 0
     d._heads = (q, o, lse, k_new, v_new, k_cache, v_cache)
     # The descriptor holds only device pointers: keep every tensor it points
     # at alive for as long as the descriptor exists, so that a caller that

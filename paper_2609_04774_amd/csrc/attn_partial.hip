@@ -124,25 +124,33 @@ struct KvSource {
   const unsigned char* v_cache;
   const int32_t* block_table;
   int P;
+  uint32_t n_blocks;
 };
+
+// Source of a cache block whose block-table entry lies outside the cache:
+// 256 zero bytes, read by every row of the block (the per-lane offset is then
+// only the 16-byte column, below 256), so such keys and values are zeros and
+// nothing outside the cache is read.
+__device__ __attribute__((aligned(256))) unsigned char g_zero_row[kHeadDim * 2];
 
 // One global_load_lds_dwordx4: lane l's 16 bytes at sbase + voff land at LDS
 // byte m0 + 16*l.  Issued as inline assembly so the compiler does not treat
 // every later LDS read as depending on it (it cannot tell the two buffers
 // apart); the kernel waits for these loads itself (vmcnt) before the barrier
-// that publishes a tile.  The base and the LDS address are wave-uniform; the
-// lane reads place them in scalar registers however the compiler carried
-// them.
+// that publishes a tile.  The LDS address is an input operand bound to m0, so
+// the compiler writes m0 itself and knows what it holds; the asm only reads
+// it, after the one wait state an m0 write needs before an LDS-DMA load.  The
+// base and the LDS address are wave-uniform; the lane reads place them in
+// scalar registers however the compiler carried them.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
   const uint64_t b = (uint64_t)(uintptr_t)sbase;
   const uint64_t bs = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32) |
                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
   asm volatile(
-      "s_mov_b32 m0, %0\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\t" ::"s"(__builtin_amdgcn_readfirstlane((int)lds_base)),
-      "v"(voff), "s"((const void*)(uintptr_t)bs)
-      : "memory", "m0");
+      "global_load_lds_dwordx4 %0, %1\n\t" ::"v"(voff), "s"((const void*)(uintptr_t)bs),
+      "{m0}"(__builtin_amdgcn_readfirstlane((int)lds_base))
+      : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
@@ -182,10 +190,16 @@ __device__ __forceinline__ TileLoad prep_tile(const Tile& x, const KvSource& src
     int lb = (x.t0 >> 4) + (row0 >> 4);
     const int last = ((x.vis + kBlockTokens - 1) >> 4) - 1;
     lb = lb < last ? lb : last;
-    const int64_t blk = ((const __attribute__((address_space(4))) int32_t*)src.block_table)[lb];
-    const int64_t base = (blk * kBlockTokens - row0) * row_stride + kvh * (kHeadDim * 2);
-    t.kb = src.k_cache + base;
-    t.vb = src.v_cache + base;
+    const int32_t blk = ((const __attribute__((address_space(4))) int32_t*)src.block_table)[lb];
+    if ((uint32_t)blk < src.n_blocks) {
+      const int64_t base = ((int64_t)blk * kBlockTokens - row0) * row_stride + kvh * (kHeadDim * 2);
+      t.kb = src.k_cache + base;
+      t.vb = src.v_cache + base;
+    } else {
+      t.kb = g_zero_row;
+      t.vb = g_zero_row;
+      t.off = lane_col;
+    }
   } else {
     const int64_t base = (int64_t)(x.t0 - src.P) * row_stride + kvh * (kHeadDim * 2);
     t.kb = src.k_new + base;
@@ -605,6 +619,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   src.v_cache = reinterpret_cast<const unsigned char*>(d.v_cache);
   src.block_table = d.block_table;
   src.P = (int)d.P;
+  src.n_blocks = (uint32_t)d.n_blocks;
 
   // Per-lane part of the tile load addresses (see prep_tile): column
   // 4(wave % 4) + lane / 16 of half wave / 4, slot lane % 16.

@@ -100,6 +100,7 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
     if (!aligned(x.k_cache, 16) || !aligned(x.v_cache, 16) || !aligned(x.block_table, 4))
       return fail(CP_ERR_INVALID, who + "k_cache/v_cache must be 16-byte and block_table 4-byte aligned");
     if (P > INT32_MAX) return fail(CP_ERR_UNSUPPORTED, who + "prefix beyond 2^31 tokens");
+    if (x.n_blocks < 1) return fail(CP_ERR_INVALID, who + "n_blocks must be >= 1 when the prefix is read");
   }
   DevDesc d;
   std::memset(&d, 0, sizeof(d));
@@ -119,6 +120,8 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
     d.local_off[i] = pl.chunk[i].local_offset;
   }
   d.prefix_keys = use_prefix ? (int32_t)P : 0;
+  // Entries are int32: a cache of more blocks than that holds every entry.
+  d.n_blocks = use_prefix ? (int32_t)std::min<int64_t>(x.n_blocks, INT32_MAX) : 0;
   d.n_seg = 0;
   if (use_suffix) {
     if (x.kv_rank == CP_KV_ALL) {
@@ -338,99 +341,109 @@ int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream)
 
 extern "C" size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_descs,
                                                  int32_t n_heads_q, int32_t n_heads_kv) {
-  Plan plan;
-  if (build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan) != CP_OK) return 0;
+  size_t total = 0;
+  const int st = guarded([&]() -> int {
+    Plan plan;
+    const int s = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
+    if (s == CP_OK) total = layout_of(plan).total;
+    return s;
+  });
+  if (st != CP_OK) return 0;
   clear_error();
-  return layout_of(plan).total;
+  return total;
 }
 
 extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
                                int32_t n_heads_kv, int32_t head_dim, float softmax_scale, void* workspace,
                                size_t workspace_bytes, void* stream) {
-  if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: head_dim must be 128");
-  if (!(softmax_scale == softmax_scale)) return fail(CP_ERR_INVALID, "cp_attn_partial: softmax_scale is NaN");
-  Plan plan;
-  int st = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
-  if (st != CP_OK) return st;
-  if (plan.items.empty()) {
-    clear_error();
-    return CP_OK;
-  }
-  const Layout lay = layout_of(plan);
-  if (!workspace) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace is NULL");
-  if (!aligned(workspace, 256)) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace must be 256-byte aligned");
-  if (workspace_bytes < lay.total)
-    return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(lay.total) + " bytes");
-  // Only the tables are uploaded; the piece slots are written by the kernel.
-  std::vector<unsigned char> host(lay.pieces, 0);
-  std::memcpy(host.data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
-  std::memcpy(host.data() + lay.items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
-  if (!plan.splits.empty())
-    std::memcpy(host.data() + lay.splits, plan.splits.data(), plan.splits.size() * sizeof(SplitItem));
-  st = stage_and_copy(host.data(), lay.pieces, workspace, (hipStream_t)stream);
-  if (st != CP_OK) return st;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
-  PartialParams p;
-  p.descs = static_cast<const DevDesc*>(workspace);
-  p.items = reinterpret_cast<const WorkItem*>(ws + lay.items);
-  p.n_items = (int32_t)plan.items.size();
-  p.Hq = n_heads_q;
-  p.Hkv = n_heads_kv;
-  p.heads_per_wg = plan.shape.heads_per_wg;
-  p.q_per_wg = plan.shape.q_per_wg;
-  p.groups_per_kv = plan.shape.groups_per_kv;
-  p.scale = scale;
-  p.scale_log2 = scale * 1.4426950408889634f;
-  p.waves_per_wg = 8;
-  p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
-  p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
-  p.n_splits = (int32_t)plan.splits.size();
-  st = launch_partial(p, stream);
-  if (st == CP_OK) clear_error();
-  return st;
+  return guarded([&]() -> int {
+    if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: head_dim must be 128");
+    if (!(softmax_scale == softmax_scale)) return fail(CP_ERR_INVALID, "cp_attn_partial: softmax_scale is NaN");
+    Plan plan;
+    int st = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
+    if (st != CP_OK) return st;
+    if (plan.items.empty()) {
+      clear_error();
+      return CP_OK;
+    }
+    const Layout lay = layout_of(plan);
+    if (!workspace) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(CP_ERR_INVALID, "cp_attn_partial: workspace must be 256-byte aligned");
+    if (workspace_bytes < lay.total)
+      return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(lay.total) + " bytes");
+    // Only the tables are uploaded; the piece slots are written by the kernel.
+    std::vector<unsigned char> host(lay.pieces, 0);
+    std::memcpy(host.data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
+    std::memcpy(host.data() + lay.items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+    if (!plan.splits.empty())
+      std::memcpy(host.data() + lay.splits, plan.splits.data(), plan.splits.size() * sizeof(SplitItem));
+    st = stage_and_copy(host.data(), lay.pieces, workspace, (hipStream_t)stream);
+    if (st != CP_OK) return st;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
+    PartialParams p;
+    p.descs = static_cast<const DevDesc*>(workspace);
+    p.items = reinterpret_cast<const WorkItem*>(ws + lay.items);
+    p.n_items = (int32_t)plan.items.size();
+    p.Hq = n_heads_q;
+    p.Hkv = n_heads_kv;
+    p.heads_per_wg = plan.shape.heads_per_wg;
+    p.q_per_wg = plan.shape.q_per_wg;
+    p.groups_per_kv = plan.shape.groups_per_kv;
+    p.scale = scale;
+    p.scale_log2 = scale * 1.4426950408889634f;
+    p.waves_per_wg = 8;
+    p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
+    p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
+    p.n_splits = (int32_t)plan.splits.size();
+    st = launch_partial(p, stream);
+    if (st == CP_OK) clear_error();
+    return st;
+  });
 }
 
 extern "C" int cp_attn_merge(int32_t n_parts, const float* const* o_parts, const float* const* lse_parts,
                              int64_t n_tokens, int32_t n_heads, int32_t head_dim, void* o_out, int32_t out_bf16,
                              float* lse_out, const cp_rank_plan* restore, void* stream) {
-  if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_merge: head_dim must be 128");
-  if (n_parts < 1 || n_parts > CP_MAX_MERGE_PARTS) return fail(CP_ERR_INVALID, "cp_attn_merge: n_parts must be 1..16");
-  if (!o_parts || !lse_parts) return fail(CP_ERR_INVALID, "cp_attn_merge: o_parts/lse_parts is NULL");
-  if (n_tokens < 0 || n_heads < 1) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens < 0 or n_heads < 1");
-  if (out_bf16 != 0 && out_bf16 != 1) return fail(CP_ERR_INVALID, "cp_attn_merge: out_bf16 must be 0 or 1");
-  MergeParams p;
-  std::memset(&p, 0, sizeof(p));
-  if (n_tokens > 0) {
-    for (int i = 0; i < n_parts; ++i) {
-      if (!o_parts[i] || !lse_parts[i]) return fail(CP_ERR_INVALID, "cp_attn_merge: NULL partial pointer");
-      if (!aligned(o_parts[i], 16) || !aligned(lse_parts[i], 4))
-        return fail(CP_ERR_INVALID, "cp_attn_merge: partial O must be 16-byte, LSE 4-byte aligned");
-      p.o[i] = o_parts[i];
-      p.lse[i] = lse_parts[i];
+  return guarded([&]() -> int {
+    if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_merge: head_dim must be 128");
+    if (n_parts < 1 || n_parts > CP_MAX_MERGE_PARTS) return fail(CP_ERR_INVALID, "cp_attn_merge: n_parts must be 1..16");
+    if (!o_parts || !lse_parts) return fail(CP_ERR_INVALID, "cp_attn_merge: o_parts/lse_parts is NULL");
+    if (n_tokens < 0 || n_heads < 1) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens < 0 or n_heads < 1");
+    if (out_bf16 != 0 && out_bf16 != 1) return fail(CP_ERR_INVALID, "cp_attn_merge: out_bf16 must be 0 or 1");
+    MergeParams p;
+    std::memset(&p, 0, sizeof(p));
+    if (n_tokens > 0) {
+      for (int i = 0; i < n_parts; ++i) {
+        if (!o_parts[i] || !lse_parts[i]) return fail(CP_ERR_INVALID, "cp_attn_merge: NULL partial pointer");
+        if (!aligned(o_parts[i], 16) || !aligned(lse_parts[i], 4))
+          return fail(CP_ERR_INVALID, "cp_attn_merge: partial O must be 16-byte, LSE 4-byte aligned");
+        p.o[i] = o_parts[i];
+        p.lse[i] = lse_parts[i];
+      }
+      if (!o_out) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out is NULL");
+      if (!aligned(o_out, 16)) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out must be 16-byte aligned");
+      if (lse_out && !aligned(lse_out, 4)) return fail(CP_ERR_INVALID, "cp_attn_merge: lse_out must be 4-byte aligned");
     }
-    if (!o_out) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out is NULL");
-    if (!aligned(o_out, 16)) return fail(CP_ERR_INVALID, "cp_attn_merge: o_out must be 16-byte aligned");
-    if (lse_out && !aligned(lse_out, 4)) return fail(CP_ERR_INVALID, "cp_attn_merge: lse_out must be 4-byte aligned");
-  }
-  if (restore) {
-    cp_rank_plan ref;
-    if (make_plan(restore->prefix_len, restore->new_len, restore->C, restore->rank, &ref) != CP_OK ||
-        !plan_equal(ref, *restore))
-      return fail(CP_ERR_INVALID, "cp_attn_merge: restore plan does not match cp_shard_plan");
-    if (restore->n_rows != n_tokens) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens != restore->n_rows");
-    p.restore = 1;
-    p.first_len = restore->chunk[0].q_len;
-    p.first_dst = restore->chunk[0].q_begin - restore->prefix_len;
-    p.second_dst = restore->chunk[1].q_begin - restore->prefix_len;
-  }
-  p.n_parts = n_parts;
-  p.n_heads = n_heads;
-  p.n_tokens = n_tokens;
-  p.o_out = o_out;
-  p.lse_out = lse_out;
-  p.out_bf16 = out_bf16;
-  int st = launch_merge(p, stream);
-  if (st == CP_OK) clear_error();
-  return st;
+    if (restore) {
+      cp_rank_plan ref;
+      if (make_plan(restore->prefix_len, restore->new_len, restore->C, restore->rank, &ref) != CP_OK ||
+          !plan_equal(ref, *restore))
+        return fail(CP_ERR_INVALID, "cp_attn_merge: restore plan does not match cp_shard_plan");
+      if (restore->n_rows != n_tokens) return fail(CP_ERR_INVALID, "cp_attn_merge: n_tokens != restore->n_rows");
+      p.restore = 1;
+      p.first_len = restore->chunk[0].q_len;
+      p.first_dst = restore->chunk[0].q_begin - restore->prefix_len;
+      p.second_dst = restore->chunk[1].q_begin - restore->prefix_len;
+    }
+    p.n_parts = n_parts;
+    p.n_heads = n_heads;
+    p.n_tokens = n_tokens;
+    p.o_out = o_out;
+    p.lse_out = lse_out;
+    p.out_bf16 = out_bf16;
+    int st = launch_merge(p, stream);
+    if (st == CP_OK) clear_error();
+    return st;
+  });
 }

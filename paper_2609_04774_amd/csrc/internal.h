@@ -5,6 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <new>
 #include <string>
 
 #include "cp_attn.h"
@@ -13,7 +14,23 @@ namespace cpattn {
 
 // Records a failure reason for cp_last_error() and returns `status`.
 int fail(int status, const std::string& why);
+// The same without allocating: `why` must be a string literal.
+int fail_static(int status, const char* why) noexcept;
 void clear_error();
+
+// Runs the body of an extern "C" entry point: a C++ exception thrown by the
+// host code (std::bad_alloc from a container, say) becomes CP_ERR_HOST
+// instead of crossing the C boundary, which would terminate the caller.
+template <class F>
+int guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail_static(CP_ERR_HOST, "out of host memory");
+  } catch (...) {
+    return fail_static(CP_ERR_HOST, "internal error (C++ exception in the host code)");
+  }
+}
 
 // Re-derives a plan from (P, R, C, rank); shared by cp_shard_plan and the
 // descriptor checks of cp_attn_partial / cp_attn_merge.
@@ -30,6 +47,8 @@ constexpr int kRowsPerWG = 256;      // (query, head) rows per workgroup
 // One descriptor as the kernel reads it.  Key sets are expressed as global
 // positions: the prefix [0, prefix_keys) through the block table, then up to
 // two suffix ranges [seg_lo, seg_hi) read from k_new / v_new row (pos - P).
+// A block-table entry outside [0, n_blocks) names no cache block: its 16
+// keys and values read as zeros.
 struct DevDesc {
   const uint16_t* q;
   const uint16_t* k_new;
@@ -48,7 +67,8 @@ struct DevDesc {
   int64_t seg_hi[2];
   int32_t n_seg;
   int32_t prefix_keys;
-  int64_t reserved;
+  int32_t n_blocks;     // blocks of k_cache / v_cache (at most 2^31 - 1)
+  int32_t reserved;
 };
 
 // One workgroup's unit: a block of query positions of one chunk of one

@@ -32,8 +32,36 @@ def test_every_declared_symbol_is_exported():
         assert hasattr(cp.lib, name), name
 
 
+def _comment_before_each_function():
+    """{function: the comment block that precedes its declaration}."""
+    with open(HEADER) as f:
+        text = f.read()
+    out = {}
+    for name in _declared_functions():
+        m = re.search(r"\n(?!\s*/?\*)[^\n]*\b" + name + r"\s*\(", text)
+        assert m, name
+        head = text[:m.start()]
+        end = head.rstrip().rfind("*/")
+        # Only a typedef may sit between the comment and the declaration.
+        between = head[end + 2:]
+        assert not between.strip() or between.strip().startswith("typedef"), name
+        start = head.rfind("/*", 0, end)
+        out[name] = " ".join(head[start + 2:end].replace("*", " ").split())
+    return out
+
+
+def test_every_declared_function_names_its_source():
+    """Each entry point's comment cites the paper section it implements, or
+    says that it is a library utility outside the paper."""
+    comments = _comment_before_each_function()
+    assert set(comments) == set(cp.EXPORTED)
+    for name, c in comments.items():
+        assert re.search(r"Sec\. \d", c) or "not from the paper" in c, name
+
+
 def test_status_strings():
-    for st in (cp.CP_OK, cp.CP_ERR_INVALID, cp.CP_ERR_UNSUPPORTED, cp.CP_ERR_HIP, cp.CP_ERR_CAPACITY):
+    for st in (cp.CP_OK, cp.CP_ERR_INVALID, cp.CP_ERR_UNSUPPORTED, cp.CP_ERR_HIP, cp.CP_ERR_CAPACITY,
+               cp.CP_ERR_HOST):
         assert cp.status_string(st) and cp.status_string(st) != "unknown status"
     assert cp.status_string(12345) == "unknown status"
 
@@ -42,7 +70,7 @@ def test_struct_layout_matches_header():
     # 4+4 + 5*8 + 2*(4+4+3*8) + 8 bytes
     assert ctypes.sizeof(cp.CpChunk) == 32
     assert ctypes.sizeof(cp.CpRankPlan) == 8 + 5 * 8 + 2 * 32 + 8
-    assert ctypes.sizeof(cp.CpPartialDesc) == ctypes.sizeof(cp.CpRankPlan) + 6 * 8 + 8 + 2 * 8
+    assert ctypes.sizeof(cp.CpPartialDesc) == ctypes.sizeof(cp.CpRankPlan) + 6 * 8 + 8 + 2 * 8 + 8
 
 
 PLAN_SWEEP = [(P, R, C) for P in (0, 16, 48, 49152) for R in (0, 1, 3, 7, 16, 100, 1024, 1000)
@@ -108,6 +136,29 @@ def test_plan_errors():
     assert cp.last_error() == ""
 
 
+def test_plan_degree_limit():
+    """C up to CP_MAX_DEGREE is planned (chunk 2C-1-rank exact); beyond it
+    every call that takes a degree refuses, instead of wrapping the chunk id."""
+    plan = cp.CpRankPlan()
+    top = cp.CP_MAX_DEGREE
+    assert cp.lib.cp_shard_plan(100, 5 * top, top, 0, ctypes.byref(plan), None, 0) == cp.CP_OK
+    assert plan.chunk[1].chunk_id == 2 * top - 1 and plan.chunk[1].q_begin == 100 + (2 * top - 1) * 3
+    for C in (top + 1, 2 ** 31 - 1):
+        assert cp.lib.cp_shard_plan(100, 5, C, 0, ctypes.byref(plan), None, 0) == cp.CP_ERR_INVALID
+        assert "CP_MAX_DEGREE" in cp.last_error()
+        a = np.zeros(8, dtype=np.int32)
+        b = np.zeros(8, dtype=np.int64)
+        assert cp.lib.cp_shard_inverse(100, 5, C, a.ctypes.data_as(ctypes.c_void_p),
+                                       b.ctypes.data_as(ctypes.c_void_p), 8) == cp.CP_ERR_INVALID
+    # A plan claiming a degree beyond the limit is refused by the merge's restore.
+    bad = cp.CpRankPlan()
+    bad.C, bad.rank, bad.prefix_len, bad.new_len = 2 ** 31 - 1, 0, 100, 5
+    optrs = (ctypes.c_void_p * 1)(FAKE)
+    lptrs = (ctypes.c_void_p * 1)(FAKE)
+    assert cp.lib.cp_attn_merge(1, optrs, lptrs, 0, 8, 128, FAKE, 0, None, ctypes.byref(bad), None) == \
+        cp.CP_ERR_INVALID
+
+
 def test_plan_length_limit_keeps_visible_pairs_exact():
     """Up to 2^31 cached and 2^31 new tokens the pair count W(R, P) =
     RP + R(R+1)/2 (Sec. 2.2) is exact in 64 bits; longer inputs are refused
@@ -142,6 +193,7 @@ def _desc(P=0, R=64, C=2, rank=0, **kw):
     d.kv_rank = kw.get("kv_rank", cp.CP_KV_ALL)
     d.o = kw.get("o", FAKE * 7)
     d.lse = kw.get("lse", FAKE * 8)
+    d.n_blocks = kw.get("n_blocks", 8)
     return d
 
 
@@ -161,6 +213,7 @@ def _partial_status(descs, Hq=8, Hkv=2, D=128, ws=FAKE * 16, ws_bytes=1 << 30):
     ("null o", {"o": None}, {}, cp.CP_ERR_INVALID),
     ("null k_new", {"k_new": None}, {}, cp.CP_ERR_INVALID),
     ("null block table with prefix", {"P": 32, "block_table": None}, {}, cp.CP_ERR_INVALID),
+    ("no cache blocks with prefix", {"P": 32, "n_blocks": 0}, {}, cp.CP_ERR_INVALID),
     ("misaligned q", {"q": FAKE + 2}, {}, cp.CP_ERR_INVALID),
     ("misaligned k_cache", {"P": 32, "k_cache": FAKE + 8}, {}, cp.CP_ERR_INVALID),
     ("include_prefix 2", {"include_prefix": 2}, {}, cp.CP_ERR_INVALID),

@@ -141,6 +141,27 @@ def test_split_key_walks_match_oracle(L, P, C, Hq, Hkv, seed):
         compare(f64(o), f64(lse), Or, Lr, f"rank 0 shard {s}")
 
 
+@pytest.mark.parametrize("L,P,C,Hq,Hkv,seed", [(400, 96, 2, 8, 2, 71), (8392, 8192, 2, 8, 2, 72)])
+def test_block_table_entries_outside_the_cache_read_as_zeros(L, P, C, Hq, Hkv, seed):
+    """Entries -1, n_blocks and 2^31 - 1 in the prefix's block table: the
+    kernel reads nothing through them and their 16 tokens act as zero keys
+    and values, as the oracle's paged gather reads them.  (400, 96): one
+    walk per item; (8392, 8192): split walks over a long prefix."""
+    prob = Problem(L, P, C, Hq, Hkv, seed)
+    bt = prob.prefix.block_table
+    n_blocks = prob.prefix.k_cache.shape[0]
+    nb = P // 16
+    for i, bad in zip((1, nb // 2, nb - 1), (-1, n_blocks, 2 ** 31 - 1)):
+        bt[i] = bad
+    for r in range(C):
+        o, lse, _, _ = prob.gpu_rank(r)
+        Or, Lr = prob.oracle_rank(r)
+        compare(f64(o), f64(lse), Or, Lr, f"rank {r}")
+    o, lse, _, _ = prob.gpu_rank(0, kv_rank=cp.CP_KV_NONE, include_prefix=True)
+    Or, Lr = prob.oracle_rank(0, kv_rank=cp.CP_KV_NONE, include_prefix=True)
+    compare(f64(o), f64(lse), Or, Lr, "prefix only")
+
+
 def test_explicit_softmax_scale():
     prob = Problem(300, 0, 2, 8, 2, 31)
     o, lse, _, _ = prob.gpu_rank(0, scale=0.05)
