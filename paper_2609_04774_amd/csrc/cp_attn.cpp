@@ -47,10 +47,6 @@ int gcd_int(int a, int b) {
   return a;
 }
 
-struct Shape {
-  int heads_per_wg, q_per_wg, groups_per_kv;
-};
-
 Shape shape_for(int Hq, int Hkv) {
   const int G = Hq / Hkv;
   Shape s;
@@ -147,16 +143,7 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
   return CP_OK;
 }
 
-struct Plan {
-  std::vector<DevDesc> descs;
-  std::vector<WorkItem> items;
-  std::vector<SplitItem> splits;
-  int64_t n_pieces = 0;
-  Shape shape;
-};
-
 constexpr int64_t kSplitBelowItems = 512;  // split only launches with fewer non-empty items
-constexpr int64_t kTargetPieces = 1024;
 constexpr int64_t kMinPieceTiles = 32;     // 1024 keys: the prologue and merge stay small
 constexpr int64_t kMaxPieces = 64;
 
@@ -182,7 +169,12 @@ int64_t item_keys(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
   return keys;
 }
 
-int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, Plan* out) {
+}  // namespace
+
+namespace cpattn {
+
+int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
+               Plan* out) {
   int st = check_heads(Hq, Hkv, "cp_attn_partial");
   if (st != CP_OK) return st;
   if (n_descs < 0) return fail(CP_ERR_INVALID, "cp_attn_partial: n_descs < 0");
@@ -223,8 +215,8 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   // Splitting pays when the longest walk is long against the piece size (the
   // pieces' set-up and the merge pass are not free).
   int64_t piece_tiles = 0;  // 0: no splitting in this launch
-  if (nonempty > 0 && nonempty < kSplitBelowItems && max_tiles >= 4 * kMinPieceTiles)
-    piece_tiles = std::max<int64_t>(kMinPieceTiles, (all_tiles + kTargetPieces - 1) / kTargetPieces);
+  if (target_pieces > 0 && nonempty > 0 && nonempty < kSplitBelowItems && max_tiles >= 4 * kMinPieceTiles)
+    piece_tiles = std::max<int64_t>(kMinPieceTiles, (all_tiles + target_pieces - 1) / target_pieces);
   out->splits.clear();
   out->n_pieces = 0;
   std::vector<std::vector<Cand>> per_xcd(kXcds);
@@ -268,12 +260,7 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   return CP_OK;
 }
 
-size_t align_up(size_t x) { return (x + kItemsAlign - 1) / kItemsAlign * kItemsAlign; }
-
-// Workspace layout: descriptors | work items | split items | piece slots.
-struct Layout {
-  size_t items, splits, pieces, total;
-};
+static size_t align_up(size_t x) { return (x + kItemsAlign - 1) / kItemsAlign * kItemsAlign; }
 
 Layout layout_of(const Plan& plan) {
   Layout l;
@@ -283,6 +270,39 @@ Layout layout_of(const Plan& plan) {
   l.total = l.pieces + (size_t)plan.n_pieces * kPieceBytes;
   return l;
 }
+
+void pack_tables(const Plan& plan, const Layout& lay, std::vector<unsigned char>* host) {
+  host->assign(lay.pieces, 0);
+  std::memcpy(host->data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
+  std::memcpy(host->data() + lay.items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+  if (!plan.splits.empty())
+    std::memcpy(host->data() + lay.splits, plan.splits.data(), plan.splits.size() * sizeof(SplitItem));
+}
+
+PartialParams partial_params(const Plan& plan, const Layout& lay, unsigned char* ws, int32_t Hq, int32_t Hkv,
+                             float scale) {
+  PartialParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.descs = reinterpret_cast<const DevDesc*>(ws);
+  p.items = reinterpret_cast<const WorkItem*>(ws + lay.items);
+  p.n_items = (int32_t)plan.items.size();
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.heads_per_wg = plan.shape.heads_per_wg;
+  p.q_per_wg = plan.shape.q_per_wg;
+  p.groups_per_kv = plan.shape.groups_per_kv;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.waves_per_wg = 8;
+  p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
+  p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
+  p.n_splits = (int32_t)plan.splits.size();
+  return p;
+}
+
+}  // namespace cpattn
+
+namespace {
 
 // Pinned host staging for the descriptor/work-list upload.  A slot is reused
 // only after the copy that read it has completed (its event).
@@ -344,7 +364,7 @@ extern "C" size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, i
   size_t total = 0;
   const int st = guarded([&]() -> int {
     Plan plan;
-    const int s = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
+    const int s = build_plan(descs, n_descs, n_heads_q, n_heads_kv, kTargetPieces, &plan);
     if (s == CP_OK) total = layout_of(plan).total;
     return s;
   });
@@ -360,7 +380,7 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
     if (head_dim != CP_HEAD_DIM) return fail(CP_ERR_UNSUPPORTED, "cp_attn_partial: head_dim must be 128");
     if (!(softmax_scale == softmax_scale)) return fail(CP_ERR_INVALID, "cp_attn_partial: softmax_scale is NaN");
     Plan plan;
-    int st = build_plan(descs, n_descs, n_heads_q, n_heads_kv, &plan);
+    int st = build_plan(descs, n_descs, n_heads_q, n_heads_kv, kTargetPieces, &plan);
     if (st != CP_OK) return st;
     if (plan.items.empty()) {
       clear_error();
@@ -372,31 +392,13 @@ extern "C" int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, in
     if (workspace_bytes < lay.total)
       return fail(CP_ERR_CAPACITY, "cp_attn_partial: workspace needs " + std::to_string(lay.total) + " bytes");
     // Only the tables are uploaded; the piece slots are written by the kernel.
-    std::vector<unsigned char> host(lay.pieces, 0);
-    std::memcpy(host.data(), plan.descs.data(), plan.descs.size() * sizeof(DevDesc));
-    std::memcpy(host.data() + lay.items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
-    if (!plan.splits.empty())
-      std::memcpy(host.data() + lay.splits, plan.splits.data(), plan.splits.size() * sizeof(SplitItem));
+    std::vector<unsigned char> host;
+    pack_tables(plan, lay, &host);
     st = stage_and_copy(host.data(), lay.pieces, workspace, (hipStream_t)stream);
     if (st != CP_OK) return st;
-    unsigned char* ws = static_cast<unsigned char*>(workspace);
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
-    PartialParams p;
-    p.descs = static_cast<const DevDesc*>(workspace);
-    p.items = reinterpret_cast<const WorkItem*>(ws + lay.items);
-    p.n_items = (int32_t)plan.items.size();
-    p.Hq = n_heads_q;
-    p.Hkv = n_heads_kv;
-    p.heads_per_wg = plan.shape.heads_per_wg;
-    p.q_per_wg = plan.shape.q_per_wg;
-    p.groups_per_kv = plan.shape.groups_per_kv;
-    p.scale = scale;
-    p.scale_log2 = scale * 1.4426950408889634f;
-    p.waves_per_wg = 8;
-    p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
-    p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
-    p.n_splits = (int32_t)plan.splits.size();
-    st = launch_partial(p, stream);
+    st = launch_partial(partial_params(plan, lay, static_cast<unsigned char*>(workspace), n_heads_q, n_heads_kv, scale),
+                        stream);
     if (st == CP_OK) clear_error();
     return st;
   });

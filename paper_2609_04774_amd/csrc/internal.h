@@ -7,6 +7,7 @@
 
 #include <new>
 #include <string>
+#include <vector>
 
 #include "cp_attn.h"
 
@@ -123,6 +124,38 @@ struct PartialParams {
 };
 
 int launch_partial(const PartialParams& p, void* stream);
+
+// Host planning of one cp_attn_partial launch (cp_attn.cpp), shared by the
+// entry points that take a caller workspace and the one that uses the
+// library's own scratch.
+struct Shape {
+  int heads_per_wg, q_per_wg, groups_per_kv;
+};
+
+struct Plan {
+  std::vector<DevDesc> descs;
+  std::vector<WorkItem> items;
+  std::vector<SplitItem> splits;
+  int64_t n_pieces = 0;
+  Shape shape;
+};
+
+// Key walks of launches with few work items are split into about
+// `target_pieces` pieces (0: never split).
+constexpr int64_t kTargetPieces = 1024;
+int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
+               Plan* out);
+
+// Workspace layout: descriptors | work items | split items | piece slots.
+// The first `pieces` bytes are uploaded from the host; the piece slots are
+// written by the kernel before they are read.
+struct Layout {
+  size_t items, splits, pieces, total;
+};
+Layout layout_of(const Plan& plan);
+void pack_tables(const Plan& plan, const Layout& lay, std::vector<unsigned char>* host);
+PartialParams partial_params(const Plan& plan, const Layout& lay, unsigned char* ws, int32_t Hq, int32_t Hkv,
+                             float scale);
 
 // ---------------------------------------------------------------------------
 // LSE merge.
