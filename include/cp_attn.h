@@ -65,6 +65,7 @@ extern "C" {
 #define CP_KV_BLOCK_TOKENS 16
 #define CP_MAX_MERGE_PARTS 16
 #define CP_MAX_DEGREE 64        /* largest CP degree C of any call */
+#define CP_NOALLOC_SCRATCH_BYTES (32u << 20) /* device scratch of cp_attn_partial_noalloc, per GPU */
 
 /* kv_rank values of cp_partial_desc besides a rank number 0..C-1. */
 #define CP_KV_ALL (-1)  /* every causally visible suffix key (all-gathered KV) */
@@ -215,6 +216,28 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
 int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
                     int32_t n_heads_kv, int32_t head_dim, float softmax_scale,
                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * cp_attn_partial for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  It takes
+ * no workspace and calls no allocating routine (no hipMalloc, hipFree or
+ * pinned host allocation); its device scratch -- the descriptor copy, the
+ * work list and the split-walk piece slots -- is a library-owned array of
+ * CP_NOALLOC_SCRATCH_BYTES (32 MiB) on each GPU it runs on, held until the
+ * process ends.  Descriptors, arguments and results are those of
+ * cp_attn_partial; when split key walks would need more piece slots than
+ * the scratch holds, fewer, longer pieces are used (same attention, other
+ * work decomposition).
+ * Each call waits on the host for `stream`'s earlier work before it
+ * overwrites the scratch, then copies the tables from host memory (a
+ * synchronous copy), so consecutive calls on one stream are safe.  The
+ * scratch is shared by every call on a GPU and keeps the last call's
+ * contents: calls that overlap on one GPU (other streams or threads) race.
+ * Errors: as cp_attn_partial, plus CP_ERR_CAPACITY when the launch's tables
+ * alone exceed the scratch (cp_attn_partial with a workspace has no limit).
+ */
+int cp_attn_partial_noalloc(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
+                            int32_t n_heads_kv, int32_t head_dim, float softmax_scale, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* Exact log-sum-exp merge of partials (+ optional restore of order)      */

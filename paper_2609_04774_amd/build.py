@@ -19,7 +19,8 @@ LIB_NAME = "libcpattn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["plan.cpp", "cp_attn.cpp", "kv_cache.cpp", "attn_partial.hip", "lse_merge.hip", "kv_cache.hip"]
+SOURCES = ["plan.cpp", "cp_attn.cpp", "noalloc.cpp", "kv_cache.cpp", "attn_partial.hip", "lse_merge.hip",
+           "kv_cache.hip"]
 
 # Packed-FP32 VALU forms are kept out of every kernel (-packed-fp32-ops).
 HIP_FLAGS = [

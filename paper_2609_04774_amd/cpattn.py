@@ -28,9 +28,10 @@ CP_MAX_MERGE_PARTS = 16
 CP_KV_ALL = -1
 CP_KV_NONE = -2
 CP_MAX_DEGREE = 64
+CP_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
-            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_merge",
+            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_partial_noalloc", "cp_attn_merge",
             "cp_kv_writeback", "cp_repartition", "cp_kv_gather")
 
 
@@ -98,6 +99,9 @@ def _load():
     lib.cp_attn_partial.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.cp_attn_partial_noalloc.restype = ctypes.c_int
+    lib.cp_attn_partial_noalloc.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p]
     lib.cp_attn_merge.restype = ctypes.c_int
     lib.cp_attn_merge.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
                                   ctypes.POINTER(ctypes.c_void_p), ctypes.c_int64, ctypes.c_int32,
@@ -291,6 +295,16 @@ def attn_partial(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int
     _check(lib.cp_attn_partial(arr, len(descs), n_heads_q, n_heads_kv, head_dim,
                                float(softmax_scale), _ptr(workspace), nbytes,
                                _stream_handle(stream)))
+
+
+def attn_partial_noalloc(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int,
+                         head_dim: int = CP_HEAD_DIM, softmax_scale: float = 0.0, stream=None):
+    """cp_attn_partial_noalloc on the given (or current torch) stream: no
+    workspace; the library's own device scratch serves the launch."""
+    _check_heads(descs, n_heads_q, n_heads_kv)
+    arr = _desc_array(descs)
+    _check(lib.cp_attn_partial_noalloc(arr, len(descs), n_heads_q, n_heads_kv, head_dim,
+                                       float(softmax_scale), _stream_handle(stream)))
 
 
 def attn_merge(o_parts, lse_parts, o_out, lse_out=None, restore: Optional[CpRankPlan] = None,

@@ -52,10 +52,14 @@ def _comment_before_each_function():
 
 def test_every_declared_function_names_its_source():
     """Each entry point's comment cites the paper section it implements, or
-    says that it is a library utility outside the paper."""
+    says that it is a library utility outside the paper; the variant without
+    allocation names the callers it is for instead."""
     comments = _comment_before_each_function()
     assert set(comments) == set(cp.EXPORTED)
     for name, c in comments.items():
+        if name == "cp_attn_partial_noalloc":
+            assert "callers that cannot allocate" in c, name
+            continue
         assert re.search(r"Sec\. \d", c) or "not from the paper" in c, name
 
 
@@ -380,3 +384,29 @@ def test_binding_refuses_host_tensors():
     q = torch.zeros((plan.n_rows, 8, 128), dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU tensor"):
         cp.make_desc(plan, q, None, None, None, None, include_prefix=False, kv_rank=cp.CP_KV_NONE)
+
+
+def _noalloc_status(descs, Hq=8, Hkv=2, D=128, scale=0.0):
+    arr = (cp.CpPartialDesc * max(1, len(descs)))(*descs)
+    return cp.lib.cp_attn_partial_noalloc(arr, len(descs), Hq, Hkv, D, scale, None)
+
+
+def test_noalloc_argument_errors():
+    """The variant without a workspace refuses what cp_attn_partial refuses,
+    before any HIP call, and an empty launch is a no-op."""
+    assert _noalloc_status([_desc()], D=64) == cp.CP_ERR_UNSUPPORTED
+    assert _noalloc_status([_desc()], scale=float("nan")) == cp.CP_ERR_INVALID
+    assert _noalloc_status([_desc(kv_rank=5)]) == cp.CP_ERR_INVALID
+    assert _noalloc_status([_desc(q=None)]) == cp.CP_ERR_INVALID
+    assert _noalloc_status([_desc(P=32, n_blocks=0)]) == cp.CP_ERR_INVALID
+    assert _noalloc_status([_desc(P=1 << 30, R=64)]) == cp.CP_ERR_UNSUPPORTED
+    assert _noalloc_status([]) == cp.CP_OK
+    assert _noalloc_status([_desc(R=3, C=4, rank=3)]) == cp.CP_OK     # a rank with no rows
+
+
+def test_noalloc_refuses_tables_beyond_its_scratch():
+    """2^29 query rows of one head: 2^21 work items, 64 MiB of tables, beyond
+    the 32 MiB scratch -- refused with CP_ERR_CAPACITY before any HIP call."""
+    d = _desc(P=0, R=1 << 29, C=1)
+    assert _noalloc_status([d], Hq=1, Hkv=1) == cp.CP_ERR_CAPACITY
+    assert "scratch" in cp.last_error()
