@@ -247,15 +247,23 @@ __device__ __forceinline__ float xsum32(float x) {
   return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
 }
 
-// Running max is only moved when it grows by more than 2^8 in the exponent
-// (per wave); until then probabilities are taken against the stale max and
-// stay below 256, which bf16 and the fp32 sums hold exactly as well.
-constexpr float kLazyRescaleLog2 = 8.f;
+// Probabilities of a tile are taken against the running max m of the tiles
+// before it, without looking at the tile's own scores first: p = 2^(x - m).
+// They stay exact relative to each other whatever their size (fp32 and bf16
+// keep 24 and 8 significant bits at any exponent), so m only has to move
+// when p could overflow.  A tile whose fp32 sum of a lane's 16 probabilities
+// exceeds 2^16 (a score more than ~2^12 above m, or the first visible key
+// of a query) is redone exactly: its scores recomputed from the K tile
+// still in LDS, their max taken, O and the sums rescaled, the probabilities
+// taken against the new max.  With probabilities below 2^16 nothing
+// overflows for any |v| below 2^100.
+constexpr float kMaxTileSum = 65536.f;
 // The running max is kept in units of the exponent (score * scale * log2 e)
 // and starts at a finite "nothing seen" value far below any real score's:
-// the first tile with a visible key then always moves it, a fully masked
-// tile (scores -inf) yields probabilities exp2(-inf) = 0 against it, and no
-// lane needs a -inf special case.
+// a query's first visible key then always overflows the check above (2^(x +
+// 1e30) = inf) and sets it exactly, a fully masked tile (scores -inf)
+// yields probabilities exp2(-inf) = 0 against it, and no lane needs a -inf
+// special case.
 constexpr float kNoMax = -1e30f;
 
 constexpr float kLn2 = 0.69314718055994531f;
@@ -368,23 +376,19 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 
 // One iteration's matrix and vector work as a fixed sequence of 16 MFMA
 // slots: slots 0-7 compute S_{j+1} = K_{j+1} Q^T (K step d = slot), slots
-// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8).  The softmax of S_j is cut into units of
-// roughly equal VALU time and dealt out over the slots, so that every MFMA
-// has vector work to overlap with; LDS fragments are read three slots ahead,
-// and the two loads of tile j+5 (K rows, then V rows) go out at slots 1 and
-// 9.  Scheduling barriers keep the slots in this order.  The other wave on
-// the same SIMD runs the same sequence shifted in time, so one wave's vector
-// and scalar work issues while the other's matrix work runs.
+// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8).  The softmax of S_j is cut
+// into units of roughly equal VALU time and dealt out over the slots, so that
+// every MFMA has vector work to overlap with; LDS fragments are read three
+// slots ahead, and the two loads of tile j+5 (K rows, then V rows) go out at
+// slots 1 and 9.  Scheduling barriers keep the slots in this order.  The other
+// wave on the same SIMD runs the same sequence shifted in time, so one wave's
+// vector and scalar work issues while the other's matrix work runs.
 //
-// Units: 0-3 running max over four scores each (scores 4u..4u+3); 4 the
-// exchange with the other lane half, the new max (in exponent units) and
-// whether any lane of the wave moved it, and the start of the sums; 5-28
-// eight times (two exponentials, one pack-and-sum) for score pairs.  The
-// rescale of the sums and of O, needed only when the max moved, follows the
-// region (rescale).
-constexpr int kUnits = 29;
+// Units: eight times (two exponentials, one pack-and-sum) for score pairs,
+// against the running max (see kMaxTileSum).  The overflow check, and the
+// exact redo of a tile in the rare case that it fails, follow the region.
 constexpr int kSlots = 16;
-constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 4, 5, 7, 9, 11, 12, 14, 16, 18, 20, 22, 23, 25, 27, 29};
+constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 3, 5, 6, 8, 9, 11, 12, 14, 15, 17, 18, 20, 21, 23, 24};
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -396,52 +400,49 @@ __device__ __forceinline__ void pin(const T& x) {
 }
 
 struct SoftmaxState {
-  float mx;       // partial max of the tile's scores
-  float m_new;    // the max after this tile (lazily moved), exponent units
   float rs;       // fp32 sum of this tile's probabilities
   float rsb;      // sum of the bf16-rounded probabilities
-  bool any_grow;  // some lane of the wave moved its max (O needs rescaling)
   bf16x2 pp[8];
 };
 
 constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
-__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float m_run, float sl2) {
-  if (u < 4) {
-    const int q = 4 * u;
-    if (q == 0)
-      st.mx = max3(__builtin_elementwise_maximum(s[0], s[1]), s[2], s[3]);
-    else
-      st.mx = max3(max3(st.mx, s[q], s[q + 1]), s[q + 2], s[q + 3]);
-    pin(st.mx);
-  } else if (u == 4) {
-    // Both lane halves hold disjoint keys of the same query and agree on the
-    // max after the exchange.  The max moves only when it grows by more than
-    // 2^8 in the exponent.
-    const float mx = xmax32(st.mx) * sl2;
-    const bool grow = mx > m_run + kLazyRescaleLog2;
-    st.m_new = grow ? mx : m_run;
-    st.any_grow = __any(grow);
-    st.rs = -0.f;  // x + -0 is x: the first add folds away
-    st.rsb = -0.f;
-    pin(st.m_new);
+// Pair t of the tile's 16 scores (registers 2t, 2t+1, already
+// exponentiated): rounded to bf16 once, and added to both sums.
+__device__ __forceinline__ void pack_and_sum(int t, const f32x16& s, SoftmaxState& st) {
+  const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
+  st.pp[t] = pp;
+  if (t == 0) {
+    st.rs = s[0] + s[1];
+    st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, 0.f, false);
   } else {
-    const int e = u - 5, t = e / 3, kind = e % 3;
-    if (kind < 2) {
-      const int i = 2 * t + kind;
-      const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i], sl2, -st.m_new));
-      pin(x);
-      s[i] = x;
-    } else {
-      const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
-      st.pp[t] = pp;
-      st.rs += s[2 * t] + s[2 * t + 1];
-      st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb, false);
-      pin(st.rs);
-      pin(st.rsb);
-      pin(pp);
-    }
+    st.rs += s[2 * t] + s[2 * t + 1];
+    st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb, false);
   }
+  pin(st.rs);
+  pin(st.rsb);
+  pin(pp);
+}
+
+__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float m_run, float sl2) {
+  const int t = u / 3, kind = u % 3;
+  if (kind < 2) {
+    const int i = 2 * t + kind;
+    const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i], sl2, -m_run));
+    pin(x);
+    s[i] = x;
+  } else {
+    pack_and_sum(t, s, st);
+  }
+}
+
+// Max of a lane's 16 scores and of the other lane half's (the same query's
+// other 16 keys), in exponent units.
+__device__ __forceinline__ float tile_max(const f32x16& s, float sl2) {
+  float mx = max3(__builtin_elementwise_maximum(s[0], s[1]), s[2], s[3]);
+#pragma unroll
+  for (int q = 4; q < 16; q += 4) mx = max3(max3(mx, s[q], s[q + 1]), s[q + 2], s[q + 3]);
+  return xmax32(mx) * sl2;
 }
 
 // Fragment g of the region: g < 8 is K step g, g >= 8 is V^T fragment
@@ -452,14 +453,14 @@ __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, cons
   return v_frag(sv, fo, (g - 8) >> 2, (g - 8) & 3);
 }
 
-// s_in: S_j (masked), turned into P_j; s_out: receives S_{j+1}.  pf: P_{j-1}
-// on entry, P_j on exit.
+// s_in: S_j (masked), turned into its probabilities against m_run (their
+// bf16 pairs and sums in st); s_out: receives S_{j+1}.  pf: P_{j-1}, added
+// into O.
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
                                                  const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
-                                                 bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB],
-                                                 f32x16 (&s_out)[kNB], float (&m_run)[kNB], float (&l_run)[kNB],
-                                                 float (&lb_run)[kNB], float sl2, const TileLoad& ld) {
-  SoftmaxState st;
+                                                 const bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB],
+                                                 f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB], float m_run, float sl2,
+                                                 const TileLoad& ld, SoftmaxState& st) {
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
@@ -474,29 +475,31 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
       o[f & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][f >> 2], o[f & 3][0], 0, 0, 0);
     }
 #pragma unroll
-    for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u)
-      softmax_unit(u, s_in[0], st, m_run[0], sl2);
+    for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u) softmax_unit(u, s_in[0], st, m_run, sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
-  // The tile's sums join the running ones; when some lane of the wave moved
-  // its max, the running sums and O are first rescaled by 2^(m_old - m_new)
-  // (exactly 1 in the lanes that did not move).
-  if (st.any_grow) {
-    const float alpha = __builtin_amdgcn_exp2f(m_run[0] - st.m_new);
-    l_run[0] = l_run[0] * alpha + st.rs;
-    lb_run[0] = lb_run[0] * alpha + st.rsb;
+}
+
+// The exact redo of tile j (rare; see kMaxTileSum): s holds S_j, recomputed
+// and masked by the caller.  The running max moves to the max of the tile
+// where that is higher, O and the running sums are rescaled by 2^(m_old -
+// m_new) (exactly 1 where it did not move, 0 before a query's first visible
+// key), and the tile's probabilities are taken against the new max.
+__device__ __forceinline__ void exact_softmax(f32x16& s, float& m_run, float& l_run, float& lb_run,
+                                              f32x16 (&o)[4][kNB], float sl2, SoftmaxState& st) {
+  const float m_new = __builtin_elementwise_maximum(tile_max(s, sl2), m_run);
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+  l_run *= alpha;
+  lb_run *= alpha;
 #pragma unroll
-    for (int db = 0; db < 4; ++db) o[db][0] *= alpha;
-  } else {
-    l_run[0] += st.rs;
-    lb_run[0] += st.rsb;
+  for (int db = 0; db < 4; ++db) o[db][0] *= alpha;
+  m_run = m_new;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) s[2 * t + k] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * t + k], sl2, -m_new));
+    pack_and_sum(t, s, st);
   }
-  m_run[0] = st.m_new;
-#pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
-    pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
-                                        __builtin_shufflevector(st.pp[4 * ks + 2], st.pp[4 * ks + 3], 0, 1, 2, 3),
-                                        0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
@@ -712,7 +715,25 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   *reinterpret_cast<u32x4*>(smem + (kBufs + ((t_first + kBufs - 1) & (kBufs - 1))) * kTileBytes + 16 * tid) =
       u32x4{};
   __syncthreads();  // the first tile is in LDS for everyone
-  if (n_tiles > 0 && wave_active) qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
+  // A tile needs masking exactly when its index lies in [mA, firstB),
+  // [mB, firstC) or [mC, n) (the thresholds below).
+  auto masked_tile = [&](int j) {
+    return (j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c;
+  };
+  auto mask_if_needed = [&](int j, f32x16 (&s)[kNB]) {
+    if (masked_tile(j)) {
+      int lim[kNB];
+      tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
+      mask_tile(s, half, lim);
+    }
+  };
+  if (n_tiles > 0 && wave_active) {
+    // The first tile's scores, and the running max seeded with their max (so
+    // that the first iteration's probabilities need no redo).
+    qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
+    mask_if_needed(t_first, sa);
+    m_run[0] = __builtin_elementwise_maximum(tile_max(sa[0], sl2), kNoMax);
+  }
 
   // Iteration j (tile buffer B = j % kBufs): mask
   // S_j, then the region (S_{j+1} from K buffer B+1, softmax of S_j, P_{j-1}
@@ -739,14 +760,26 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   };
   auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
     const int B = j & (kBufs - 1);
-    if ((j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c) {
-      int lim[kNB];
-      tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
-      mask_tile(s_in, half, lim);
-    }
+    mask_if_needed(j, s_in);
     const TileLoad ld = next_load(j);
+    SoftmaxState st;
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
-                     pf, o, s_in, s_out, m_run, l_run, lb_run, sl2, ld);
+                     pf, o, s_in, s_out, m_run[0], sl2, ld, st);
+    // Rare: some lane's probabilities were too large (its max grew by more
+    // than ~2^12, or it saw its first key).  Redo the tile exactly; its K
+    // tile is still in buffer B (tile j + 8 is loaded three iterations on).
+    if (__builtin_amdgcn_ballot_w64(!(st.rs <= kMaxTileSum)) != 0) {
+      qk_tile(smem + B * kTileBytes, fo, qf, s_in);
+      mask_if_needed(j, s_in);
+      exact_softmax(s_in[0], m_run[0], l_run[0], lb_run[0], o, sl2, st);
+    }
+    l_run[0] += st.rs;
+    lb_run[0] += st.rsb;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+      pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
+                                          __builtin_shufflevector(st.pp[4 * ks + 2], st.pp[4 * ks + 3], 0, 1, 2, 3),
+                                          0, 1, 2, 3, 4, 5, 6, 7);
   };
 
   // Iterations go in pairs behind one barrier.  At a pair's start every tile
