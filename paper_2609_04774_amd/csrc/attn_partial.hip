@@ -23,10 +23,10 @@
 //     row max and row sum are in-lane plus one exchange with lane ^ 32, and
 //     the probabilities feed O^T += V^T P^T directly from registers.  V^T
 //     fragments come from the key-major V tile through ds_read_b64_tr_b16.
-//   * Software pipeline: iteration j runs S_{j+1} = K_{j+1} Q^T, the softmax
-//     of S_j and O += V_{j-1}^T P_{j-1} -- three independent streams -- as
-//     one fixed sequence of MFMA slots with the softmax dealt out between
-//     them.  Iterations go in pairs that share one workgroup barrier and swap
+//   * Software pipeline: iteration j runs O += V_{j-1}^T P_{j-1}, the
+//     softmax of S_j and S_{j+1} = K_{j+1} Q^T -- three independent streams
+//     -- as one fixed sequence of MFMA slots with the softmax dealt out
+//     between them.  Iterations go in pairs that share one workgroup barrier and swap
 //     the two score register sets; each iteration loads tile j+5 into LDS.
 //   * LDS tiles are stored by 16-key halves and 16-byte columns: column c of
 //     a half holds head-dim chunk c (8 values) of its 16 keys, key k at slot
@@ -375,14 +375,18 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 }
 
 // One iteration's matrix and vector work as a fixed sequence of 16 MFMA
-// slots: slots 0-7 compute S_{j+1} = K_{j+1} Q^T (K step d = slot), slots
-// 8-15 add P_{j-1} V_{j-1} (V fragment slot - 8).  The softmax of S_j is cut
-// into units of roughly equal VALU time and dealt out over the slots, so that
-// every MFMA has vector work to overlap with; LDS fragments are read three
-// slots ahead, and the two loads of tile j+5 (K rows, then V rows) go out at
-// slots 1 and 9.  Scheduling barriers keep the slots in this order.  The other
-// wave on the same SIMD runs the same sequence shifted in time, so one wave's
-// vector and scalar work issues while the other's matrix work runs.
+// slots: slots 0-7 add P_{j-1} V_{j-1} (V fragment = slot: k-step slot/4,
+// d-block slot%4), slots 8-15 compute S_{j+1} = K_{j+1} Q^T (K step slot -
+// 8).  The softmax of S_j is cut into units of roughly equal VALU time and
+// dealt out over the slots, so that every MFMA has vector work to overlap
+// with.  LDS fragments are read three slots ahead in one continuous stream:
+// the last three slots read the next iteration's first V fragments (of tile
+// j, published since before this pair of iterations), so no iteration starts
+// by waiting for a fresh LDS read.  The two loads of tile j+5 (K rows, then
+// V rows) go out at slots 1 and 9.  Scheduling barriers keep the slots in
+// this order.  The other wave on the same SIMD runs the same sequence
+// shifted in time, so one wave's vector and scalar work issues while the
+// other's matrix work runs.
 //
 // Units: eight times (two exponentials, one pack-and-sum) for score pairs,
 // against the running max (see kMaxTileSum).  The overflow check, and the
@@ -445,34 +449,38 @@ __device__ __forceinline__ float tile_max(const f32x16& s, float sl2) {
   return xmax32(mx) * sl2;
 }
 
-// Fragment g of the region: g < 8 is K step g, g >= 8 is V^T fragment
-// (k-step (g-8)/4, d-block (g-8)%4).
+// Fragment g of the region: g < 8 is V^T fragment (k-step g/4, d-block
+// g%4), g >= 8 is K step g - 8.
 __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, const unsigned char* sk,
                                             const FragOffsets& fo) {
-  if (g < 8) return *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, g));
-  return v_frag(sv, fo, (g - 8) >> 2, (g - 8) & 3);
+  if (g < 8) return v_frag(sv, fo, g >> 2, g & 3);
+  return *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, g - 8));
 }
 
 // s_in: S_j (masked), turned into its probabilities against m_run (their
 // bf16 pairs and sums in st); s_out: receives S_{j+1}.  pf: P_{j-1}, added
 // into O.
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
-                                                 const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
-                                                 const bf16x8 (&pf)[kNB][2], f32x16 (&o)[4][kNB],
-                                                 f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB], float m_run, float sl2,
-                                                 const TileLoad& ld, SoftmaxState& st) {
+                                                 const unsigned char* sv_next, const FragOffsets& fo,
+                                                 const bf16x8 (&qf)[kNB][8], const bf16x8 (&pf)[kNB][2],
+                                                 f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB],
+                                                 float m_run, float sl2, const TileLoad& ld, SoftmaxState& st,
+                                                 bf16x8 (&pre)[kLookahead]) {
   bf16x8 fr[16];
 #pragma unroll
-  for (int g = 0; g < kLookahead; ++g) fr[g] = load_frag(g, sv, sk, fo);
+  for (int g = 0; g < kLookahead; ++g) fr[g] = pre[g];
 #pragma unroll
   for (int slot = 0; slot < kSlots; ++slot) {
-    if (slot + kLookahead < 16) fr[slot + kLookahead] = load_frag(slot + kLookahead, sv, sk, fo);
+    const int g = slot + kLookahead;
+    if (g < 16)
+      fr[g] = load_frag(g, sv, sk, fo);
+    else
+      pre[g - 16] = load_frag(g - 16, sv_next, sk, fo);  // the next iteration's first V fragments
     if ((slot & 7) == 1) issue_load(ld, slot >> 3);
     if (slot < 8) {
-      mfma_qk(s_out[0], fr[slot], qf[0][slot], slot == 0);
+      o[slot & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][slot >> 2], o[slot & 3][0], 0, 0, 0);
     } else {
-      const int f = slot - 8;
-      o[f & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][f >> 2], o[f & 3][0], 0, 0, 0);
+      mfma_qk(s_out[0], fr[slot], qf[0][slot - 8], slot == 8);
     }
 #pragma unroll
     for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u) softmax_unit(u, s_in[0], st, m_run, sl2);
@@ -727,7 +735,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       mask_tile(s, half, lim);
     }
   };
+  bf16x8 pre[kLookahead];
   if (n_tiles > 0 && wave_active) {
+#pragma unroll
+    for (int g = 0; g < kLookahead; ++g)
+      pre[g] = load_frag(g, smem + ((t_first + kBufs - 1) & (kBufs - 1)) * kTileBytes, smem, fo);
     // The first tile's scores, and the running max seeded with their max (so
     // that the first iteration's probabilities need no redo).
     qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
@@ -763,8 +775,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     mask_if_needed(j, s_in);
     const TileLoad ld = next_load(j);
     SoftmaxState st;
-    pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes, fo, qf,
-                     pf, o, s_in, s_out, m_run[0], sl2, ld, st);
+    pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes,
+                     smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run[0], sl2, ld, st, pre);
     // Rare: some lane's probabilities were too large (its max grew by more
     // than ~2^12, or it saw its first key).  Redo the tile exactly; its K
     // tile is still in buffer B (tile j + 8 is loaded three iterations on).
