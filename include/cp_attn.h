@@ -321,6 +321,31 @@ int cp_repartition(int64_t P, int64_t R, int32_t C_src, const void* const* src_r
                    int32_t dst_rank, void* dst_rows, int64_t row_bytes, void* stream);
 
 /*
+ * cp_repartition for every destination rank at once, and for up to two row
+ * sets (a request's K and V) in one launch (Sec. 6.2: after a split or merge
+ * the resident KV is installed under the new CP geometry; Sec. 7.2:
+ * inter-degree replication repartitions KV states for the destination).
+ * Row t of set k of destination rank r receives the row of the same global
+ * position from the degree-C_src rank that holds it, as cp_repartition(P, R,
+ * C_src, set k's sources, C_dst, r, ...) would write it.
+ *   src_rows   host array of n_sets * C_src device pointers: entry
+ *              k * C_src + r is set k's rows of source rank r
+ *              ([n_rows_r][row_bytes], plan order; NULL allowed for a rank
+ *              with no rows).  16-byte aligned.
+ *   dst_rows   host array of n_sets * C_dst device pointers: entry
+ *              k * C_dst + r receives set k's rows of destination rank r
+ *              ([n_rows_r][row_bytes]); no destination may overlap a source
+ *              or another destination.  NULL allowed for a rank with no rows.
+ *   n_sets     1 or 2.
+ *   row_bytes  bytes per row, a positive multiple of 16.
+ *   1 <= C_src, C_dst <= CP_MAX_DEGREE.  R == 0 is a no-op.
+ * Errors: CP_ERR_INVALID, CP_ERR_UNSUPPORTED (positions beyond 2^31),
+ * CP_ERR_HIP.
+ */
+int cp_repartition_all(int64_t P, int64_t R, int32_t C_src, const void* const* src_rows, int32_t C_dst,
+                       void* const* dst_rows, int32_t n_sets, int64_t row_bytes, void* stream);
+
+/*
  * Paged KV gather: copies positions pos_begin .. pos_begin + n_tokens - 1 of
  * one request out of the block-16 paged cache into contiguous rows.  It is
  * the read side of cp_kv_writeback and the same block-table gather that

@@ -32,7 +32,7 @@ CP_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
             "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_partial_noalloc", "cp_attn_merge",
-            "cp_kv_writeback", "cp_repartition", "cp_kv_gather")
+            "cp_kv_writeback", "cp_repartition", "cp_repartition_all", "cp_kv_gather")
 
 
 class CpChunk(ctypes.Structure):
@@ -115,6 +115,11 @@ def _load():
     lib.cp_repartition.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                    ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_int32,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.cp_repartition_all.restype = ctypes.c_int
+    lib.cp_repartition_all.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                       ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32,
+                                       ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_int64,
+                                       ctypes.c_void_p]
     lib.cp_kv_gather.restype = ctypes.c_int
     lib.cp_kv_gather.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                  ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
@@ -394,3 +399,29 @@ def repartition(prefix_len: int, new_len: int, src_rows, C_dst: int, dst_rank: i
     row_bytes = math.prod(dst_rows.shape[1:]) * dst_rows.element_size()
     _check(lib.cp_repartition(prefix_len, new_len, C_src, ptrs, C_dst, dst_rank, _ptr(dst_rows), row_bytes,
                               _stream_handle(stream)))
+
+
+def repartition_all(prefix_len: int, new_len: int, src_sets, dst_sets, stream=None):
+    """cp_repartition_all of torch device tensors: src_sets[k] is the list of
+    the C_src ranks' row tensors of set k (plan order), dst_sets[k] the list of
+    the C_dst destination ranks' tensors it fills -- every destination rank of
+    up to two sets (K and V) in one launch."""
+    n_sets = len(src_sets)
+    if n_sets != len(dst_sets) or n_sets not in (1, 2):
+        raise ValueError("src_sets and dst_sets must both hold 1 or 2 sets")
+    C_src, C_dst = len(src_sets[0]), len(dst_sets[0])
+    ref = dst_sets[0][0]
+    for k in range(n_sets):
+        if len(src_sets[k]) != C_src or len(dst_sets[k]) != C_dst:
+            raise ValueError("every set needs C_src sources and C_dst destinations")
+        for r, t in enumerate(src_sets[k]):
+            pl, _ = shard_plan(prefix_len, new_len, C_src, r, with_rows=False)
+            _dev(t, f"src_sets[{k}][{r}]", ref.dtype, pl.n_rows, tuple(ref.shape[1:]))
+        for r, t in enumerate(dst_sets[k]):
+            pl, _ = shard_plan(prefix_len, new_len, C_dst, r, with_rows=False)
+            _dev(t, f"dst_sets[{k}][{r}]", ref.dtype, pl.n_rows, tuple(ref.shape[1:]))
+    srcs = (ctypes.c_void_p * (n_sets * C_src))(*[_ptr(t) if t.numel() else None for st in src_sets for t in st])
+    dsts = (ctypes.c_void_p * (n_sets * C_dst))(*[_ptr(t) if t.numel() else None for st in dst_sets for t in st])
+    row_bytes = math.prod(ref.shape[1:]) * ref.element_size()
+    _check(lib.cp_repartition_all(prefix_len, new_len, C_src, srcs, C_dst, dsts, n_sets, row_bytes,
+                                  _stream_handle(stream)))

@@ -210,6 +210,21 @@ struct RepartitionParams {
 
 int launch_repartition(const RepartitionParams& p, void* stream);
 
+// Every destination rank of up to two row sets in one launch: row i of the
+// suffix (global position P + i) of set k goes from its source rank to its
+// destination rank, both found in closed form from the two zigzag plans.
+struct RepartitionAllParams {
+  const unsigned char* src[2][CP_MAX_DEGREE];
+  unsigned char* dst[2][CP_MAX_DEGREE];
+  int64_t row_bytes;
+  int64_t R;
+  int64_t s_src, s_dst;         // chunk lengths at the two degrees
+  int32_t C_src, C_dst;
+  int32_t n_sets;
+};
+
+int launch_repartition_all(const RepartitionAllParams& p, void* stream);
+
 struct GatherParams {
   const unsigned char* k_cache;  // [n_blocks][16][row_bytes]
   const unsigned char* v_cache;

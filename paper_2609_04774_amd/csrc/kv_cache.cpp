@@ -103,6 +103,52 @@ extern "C" int cp_repartition(int64_t P, int64_t R, int32_t C_src, const void* c
   });
 }
 
+extern "C" int cp_repartition_all(int64_t P, int64_t R, int32_t C_src, const void* const* src_rows, int32_t C_dst,
+                                  void* const* dst_rows, int32_t n_sets, int64_t row_bytes, void* stream) {
+  return guarded([&]() -> int {
+    const std::string who = "cp_repartition_all: ";
+    if (C_src < 1 || C_src > CP_MAX_DEGREE || C_dst < 1 || C_dst > CP_MAX_DEGREE)
+      return fail(CP_ERR_INVALID, who + "degrees must be 1..64");
+    if (n_sets < 1 || n_sets > 2) return fail(CP_ERR_INVALID, who + "n_sets must be 1 or 2");
+    if (row_bytes <= 0 || row_bytes % 16)
+      return fail(CP_ERR_INVALID, who + "row_bytes must be a positive multiple of 16");
+    if (P < 0 || R < 0) return fail(CP_ERR_INVALID, who + "P and R must be >= 0");
+    if (P + R > ((int64_t)1 << 31)) return fail(CP_ERR_UNSUPPORTED, who + "positions beyond 2^31");
+    if (R > 0 && (!src_rows || !dst_rows)) return fail(CP_ERR_INVALID, who + "src_rows / dst_rows is NULL");
+    RepartitionAllParams p;
+    std::memset(&p, 0, sizeof(p));
+    cp_rank_plan pl;
+    for (int k = 0; k < n_sets && R > 0; ++k) {
+      for (int r = 0; r < C_src; ++r) {
+        if (make_plan(P, R, C_src, r, &pl) != CP_OK) return fail(CP_ERR_INVALID, who + "invalid (P, R, C_src)");
+        const void* ptr = src_rows[k * C_src + r];
+        if (pl.n_rows > 0 && (!ptr || !aligned(ptr, 16)))
+          return fail(CP_ERR_INVALID, who + "source set " + std::to_string(k) + " rank " + std::to_string(r) +
+                                          " rows NULL or not 16-byte aligned");
+        p.src[k][r] = static_cast<const unsigned char*>(ptr);
+        p.s_src = pl.chunk_len;
+      }
+      for (int r = 0; r < C_dst; ++r) {
+        if (make_plan(P, R, C_dst, r, &pl) != CP_OK) return fail(CP_ERR_INVALID, who + "invalid (P, R, C_dst)");
+        void* ptr = dst_rows[k * C_dst + r];
+        if (pl.n_rows > 0 && (!ptr || !aligned(ptr, 16)))
+          return fail(CP_ERR_INVALID, who + "destination set " + std::to_string(k) + " rank " + std::to_string(r) +
+                                          " rows NULL or not 16-byte aligned");
+        p.dst[k][r] = static_cast<unsigned char*>(ptr);
+        p.s_dst = pl.chunk_len;
+      }
+    }
+    p.row_bytes = row_bytes;
+    p.R = R;
+    p.C_src = C_src;
+    p.C_dst = C_dst;
+    p.n_sets = n_sets;
+    const int st = launch_repartition_all(p, stream);
+    if (st == CP_OK) clear_error();
+    return st;
+  });
+}
+
 extern "C" int cp_kv_gather(const void* k_cache, const void* v_cache, int64_t n_blocks, const int32_t* block_table,
                             int64_t table_len, int64_t pos_begin, int64_t n_tokens, int32_t n_heads_kv,
                             int32_t head_dim, void* k_rows, void* v_rows, void* stream) {

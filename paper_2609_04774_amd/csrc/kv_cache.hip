@@ -86,6 +86,40 @@ __global__ __launch_bounds__(kThreads) void repartition_kernel(RepartitionParams
   }
 }
 
+// Where suffix index i sits at degree C with chunk length s: the rank holding
+// its chunk c (rank c or 2C-1-c) and the local row there (after that rank's
+// first chunk when c is its second).
+struct RankRow {
+  int64_t rank, row;
+};
+
+__device__ __forceinline__ RankRow rank_row(int64_t i, int64_t C, int64_t s, int64_t R) {
+  const int64_t c = i / s;
+  const int64_t r = c < C ? c : 2 * C - 1 - c;
+  int64_t local = i - c * s;
+  if (c != r) {
+    const int64_t first = R - r * s;  // rows of rank r's first chunk
+    local += first < 0 ? 0 : (first > s ? s : first);
+  }
+  return RankRow{r, local};
+}
+
+// One wave per (set, suffix index): the row moves from its source rank to its
+// destination rank.
+__global__ __launch_bounds__(kThreads) void repartition_all_kernel(RepartitionAllParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int k = wave; k < kRowsPerGroup; k += kWaves) {
+    const int64_t t = (int64_t)blockIdx.x * kRowsPerGroup + k;
+    if (t >= p.n_sets * p.R) break;
+    const int set = t >= p.R ? 1 : 0;
+    const int64_t i = t - set * p.R;
+    const RankRow from = rank_row(i, p.C_src, p.s_src, p.R);
+    const RankRow to = rank_row(i, p.C_dst, p.s_dst, p.R);
+    copy_row(p.src[set][from.rank] + from.row * p.row_bytes, p.dst[set][to.rank] + to.row * p.row_bytes,
+             p.row_bytes, lane);
+  }
+}
+
 // One wave gathers one row of K and one of V out of the paged cache: per
 // round, up to four 16-byte pieces of each (lane l takes pieces l, l+64, ...)
 // are loaded before any is stored, with non-temporal hints (every byte is
@@ -132,6 +166,16 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(GatherParams p) {
 }
 
 }  // namespace
+
+int launch_repartition_all(const RepartitionAllParams& p, void* stream) {
+  const int64_t rows = p.n_sets * p.R;
+  if (rows == 0) return CP_OK;
+  const int64_t groups = (rows + kRowsPerGroup - 1) / kRowsPerGroup;
+  hipLaunchKernelGGL(repartition_all_kernel, dim3((unsigned)groups), dim3(kThreads), 0, (hipStream_t)stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_repartition_all launch: ") + hipGetErrorString(e));
+  return CP_OK;
+}
 
 int launch_gather(const GatherParams& p, void* stream) {
   if (p.n_rows == 0) return CP_OK;

@@ -410,3 +410,28 @@ def test_noalloc_refuses_tables_beyond_its_scratch():
     d = _desc(P=0, R=1 << 29, C=1)
     assert _noalloc_status([d], Hq=1, Hkv=1) == cp.CP_ERR_CAPACITY
     assert "scratch" in cp.last_error()
+
+
+def _rpa_status(P=0, R=64, C_src=2, C_dst=4, n_sets=2, row_bytes=512, src=None, dst=None):
+    n_src = max(1, n_sets) * C_src
+    n_dst = max(1, n_sets) * C_dst
+    s = (ctypes.c_void_p * n_src)(*([FAKE] * n_src if src is None else src))
+    d = (ctypes.c_void_p * n_dst)(*([FAKE * 2] * n_dst if dst is None else dst))
+    return cp.lib.cp_repartition_all(P, R, C_src, s, C_dst, d, n_sets, row_bytes, None)
+
+
+def test_repartition_all_argument_errors():
+    """Every refusal happens before any HIP call."""
+    assert _rpa_status(C_src=0) == cp.CP_ERR_INVALID
+    assert _rpa_status(C_dst=65) == cp.CP_ERR_INVALID
+    assert _rpa_status(n_sets=3) == cp.CP_ERR_INVALID
+    assert _rpa_status(n_sets=0) == cp.CP_ERR_INVALID
+    assert _rpa_status(row_bytes=24) == cp.CP_ERR_INVALID
+    assert _rpa_status(P=-1) == cp.CP_ERR_INVALID
+    assert _rpa_status(P=1 << 31, R=1) == cp.CP_ERR_UNSUPPORTED
+    # A rank with rows needs an aligned pointer, in either set.
+    assert _rpa_status(src=[FAKE, FAKE, FAKE, None]) == cp.CP_ERR_INVALID
+    assert _rpa_status(dst=[FAKE * 2] * 7 + [FAKE + 8]) == cp.CP_ERR_INVALID
+    assert "set 1 rank 3" in cp.last_error()
+    # R < 2C: ranks without rows may be NULL; R = 0 launches nothing.
+    assert _rpa_status(R=0, src=[None] * 4, dst=[None] * 8) == cp.CP_OK

@@ -142,6 +142,45 @@ def test_repartition_matches_oracle(P, R, C_src, C_dst):
         assert np.array_equal(f64(dst), np.asarray(want[r]).reshape(f64(dst).shape))
 
 
+@pytest.mark.parametrize("P,R,C_src,C_dst", [(0, 64, 2, 4), (16, 37, 4, 2), (0, 70, 3, 5), (32, 8, 1, 4),
+                                               (0, 1000, 8, 1), (48, 5, 4, 8)])
+def test_repartition_all_matches_oracle(P, R, C_src, C_dst):
+    """Every destination rank of two row sets (K and V) in one launch, bit for
+    bit the oracle's re-shard of each set."""
+    g = synth.generator(3450 + R, device=DEV)
+    sets = [synth.randn_bf16(g, (R, 2, 128), device=DEV) for _ in range(2)]
+    src = [_ranks(x, P, R, C_src) for x in sets]
+    dst = [[torch.full((cp.shard_plan(P, R, C_dst, r)[0].n_rows, 2, 128), float("nan"), dtype=torch.bfloat16,
+                       device=DEV) for r in range(C_dst)] for _ in range(2)]
+    cp.repartition_all(P, R, src, dst)
+    torch.cuda.synchronize()
+    for k in range(2):
+        want = ocache.repartition(P, R, C_src, [f64(t) for t in src[k]], C_dst)
+        for r in range(C_dst):
+            assert np.array_equal(f64(dst[k][r]), np.asarray(want[r]).reshape(f64(dst[k][r]).shape)), (k, r)
+
+
+def test_repartition_all_full_size_round_trip():
+    """The 32K Llama-3-8B request's K and V, 4 -> 8 -> 4 ranks, one launch each
+    way: every degree-8 rank holds its own rows, and the way back restores the
+    degree-4 ranks exactly."""
+    w = synth.WORKLOADS["llama3_8b_32k_c4"]
+    g = synth.generator(3550, device=DEV)
+    kv = [synth.randn_bf16(g, (w.R, w.Hkv, w.D), device=DEV) for _ in range(2)]
+    src = [_ranks(x, 0, w.R, 4) for x in kv]
+    mid = [[torch.empty((cp.shard_plan(0, w.R, 8, r)[0].n_rows, w.Hkv, w.D), dtype=torch.bfloat16, device=DEV)
+            for r in range(8)] for _ in range(2)]
+    cp.repartition_all(0, w.R, src, mid)
+    back = [[torch.empty_like(t) for t in src[k]] for k in range(2)]
+    cp.repartition_all(0, w.R, mid, back)
+    torch.cuda.synchronize()
+    for k in range(2):
+        for r in range(8):
+            assert torch.equal(mid[k][r], _rank_rows(kv[k], 0, w.R, 8, r))
+        for r in range(4):
+            assert torch.equal(back[k][r], src[k][r])
+
+
 def test_repartition_full_size_round_trip():
     """32K Llama-3-8B K rows re-sharded 4 -> 8 -> 4 ranks; degree-8 ranks 2k
     and 2k+1 hold exactly the rows of degree-4 rank k."""
