@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--hetero", action="store_true",
                     help="also time the heterogeneous batch (64 requests, one varlen launch); off by default so "
                          "that a kernel trace of the default run holds only the workload's attention launches")
+    ap.add_argument("--c-rule", choices=["cost", "length", "both"], default="both",
+                    help="per-request CP degree of the heterogeneous batch: the placement cost over the "
+                         "calibrated prefill-time model, the fixed length rule, or both (each timed)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-clock budget of the CPU oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -97,65 +100,85 @@ def measured_traffic(workload, mode="allgather"):
     return None if f is None else f["traffic"]
 
 
+CALIBRATION = os.path.join(ROOT, "profiles", "calibration_attention_llama3_8b.json")
+
+
 def heterogeneous_batch(args, gen, dev, stream, reps=5):
     """The varlen launch: 64 requests of lognormal length (median 2048, clipped
-    to 256..131072), each with its CP degree by length bucket, 19 of them with
-    a cached prefix in one shared paged pool -- every (request, rank) shard's
-    partial over all its visible keys in one cp_attn_partial launch."""
+    to 256..131072), 19 of them with a cached prefix in one shared paged pool
+    -- every (request, rank) shard's partial over all its visible keys in one
+    cp_attn_partial launch.  Each request's CP degree comes from the placement
+    cost (PreferDegree over the calibrated prefill-time model) and, for
+    comparison, from the fixed length rule; the same seeded data is run under
+    each rule chosen by --c-rule."""
     import torch
 
     import synth
     from paper_2609_04774_amd import cpattn as cp
+    from paper_2609_04774_amd import placement as pl
 
     Hq, Hkv, D, B = 32, 8, 128, synth.BLOCK_TOKENS
     reqs = synth.hetero_requests()
-    total_blocks = sum(P // B for _, P, _ in reqs) + 32
+    model = pl.model_from_calibration(CALIBRATION)
+    total_blocks = sum(P // B for _, P in reqs) + 32
     k_pool = synth.randn_bf16(gen, (total_blocks, B, Hkv, D), device="cuda")
     v_pool = synth.randn_bf16(gen, (total_blocks, B, Hkv, D), device="cuda")
     free = torch.randperm(total_blocks, generator=gen, device="cuda")
     used = 0
-    keep, descs = [], []
-    pairs = 0
-    for L, P, C in reqs:
+    data = []
+    for L, P in reqs:
         R = L - P
-        k = synth.randn_bf16(gen, (R, Hkv, D), device="cuda")
-        v = synth.randn_bf16(gen, (R, Hkv, D), device="cuda")
+        q_full, k, v = synth.qkv(gen, R, R, Hq, Hkv, D, device="cuda")
         table = None
         if P:
             pre = synth.paged_prefix(gen, P, Hkv, D, device="cuda",
                                      pool=(k_pool, v_pool, free[used:used + P // B]))
             used += P // B
             table = pre.block_table
-        for r in range(C):
-            plan, _ = cp.shard_plan(P, R, C, r, with_rows=False)
-            if plan.n_rows == 0:
-                continue
-            q = synth.randn_bf16(gen, (plan.n_rows, Hq, D), device="cuda")
-            o = torch.empty((plan.n_rows, Hq, D), dtype=torch.float32, device=dev)
-            lse = torch.empty((plan.n_rows, Hq), dtype=torch.float32, device=dev)
-            descs.append(cp.make_desc(plan, q, k, v, o, lse, k_pool, v_pool, table, include_prefix=True))
-            keep.append((q, k, v, o, lse, table))
-            pairs += plan.visible_pairs
-    ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=dev)
-    for _ in range(2):
-        cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
-    torch.cuda.synchronize()
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for _ in range(reps):
-        cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
-    b.record(stream)
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / reps
-    flop = 4.0 * D * Hq * pairs
+        data.append((L, P, R, q_full, k, v, table))
     out = {
-        "kernel": "attn_partial_kernel", "requests": len(reqs), "tokens": sum(L for L, _, _ in reqs),
-        "prefixed": sum(1 for _, P, _ in reqs if P), "descriptors": len(descs), "flop": flop,
-        "ms": round(ms, 4), "TFLOP_s": round(flop / (ms * 1e-3) / 1e12, 2),
-        "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kernel": "attn_partial_kernel", "requests": len(reqs), "tokens": sum(L for L, _ in reqs),
+        "prefixed": sum(1 for _, P in reqs if P),
+        "degree_model": {"source": os.path.relpath(CALIBRATION, ROOT), "d0_s": model.d, "alpha_s": model.alpha,
+                         "beta": pl.DEFAULT_BETA, "lambda": pl.DEFAULT_LAMBDA},
     }
-    del keep, descs, ws, k_pool, v_pool
+    rules = ["cost", "length"] if args.c_rule == "both" else [args.c_rule]
+    for rule in rules:
+        degrees = pl.choose_degrees(reqs, rule, model)
+        keep, descs = [], []
+        pairs = 0
+        for (L, P, R, q_full, k, v, table), C in zip(data, degrees):
+            for r in range(C):
+                plan, rows = cp.shard_plan(P, R, C, r)
+                if plan.n_rows == 0:
+                    continue
+                q = q_full[torch.as_tensor(rows - P, device=dev)].contiguous()
+                o = torch.empty((plan.n_rows, Hq, D), dtype=torch.float32, device=dev)
+                lse = torch.empty((plan.n_rows, Hq), dtype=torch.float32, device=dev)
+                descs.append(cp.make_desc(plan, q, k, v, o, lse, k_pool, v_pool, table, include_prefix=True))
+                keep.append((q, o, lse))
+                pairs += plan.visible_pairs
+        ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=dev)
+        for _ in range(2):
+            cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        flop = 4.0 * D * Hq * pairs
+        out[rule] = {
+            "C_histogram": {str(C): degrees.count(C) for C in pl.DEGREES},
+            "descriptors": len(descs), "flop": flop, "ms": round(ms, 4),
+            "TFLOP_s": round(flop / (ms * 1e-3) / 1e12, 2),
+            "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        }
+        del keep, descs, ws
+    del data, k_pool, v_pool
     return out
 
 
@@ -337,9 +360,8 @@ def main():
     dst_v = [torch.empty_like(t) for t in dst_k]
 
     def reshard():
-        for r in range(2 * C):
-            cp.repartition(P, R, k_ranks, 2 * C, r, dst_k[r], stream=stream)
-            cp.repartition(P, R, v_ranks, 2 * C, r, dst_v[r], stream=stream)
+        # Every degree-2C rank's K and V rows in one launch.
+        cp.repartition_all(P, R, [k_ranks, v_ranks], [dst_k, dst_v], stream=stream)
 
     rp_ms = timed(reshard)
     rp_bytes = 2 * 2 * R * Hkv * D * 2                # K and V rows, read once and written once
@@ -416,10 +438,11 @@ def main():
         },
         "heterogeneous_batch": hetero,
         "repartition": {
-            "kernel": "repartition_kernel", "bound": "hbm", "ms": round(rp_ms, 4), "bytes": rp_bytes,
+            "kernel": "repartition_all_kernel", "bound": "hbm", "ms": round(rp_ms, 4), "bytes": rp_bytes,
             "GB_s": round(rp_bytes / (rp_ms * 1e-3) / 1e9, 1),
             "frac": round(rp_bytes / (rp_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "what": "the request's K and V rows re-sharded from degree C to degree 2C (4C launches)",
+            "what": "the request's K and V rows re-sharded from degree C to degree 2C, every destination "
+                    "rank in one launch (cp_repartition_all)",
         },
         "cpu_baseline": cpu,
         "parity_sample": parity,
@@ -440,6 +463,16 @@ def cpu_baseline(args, w, plan, rows, q, k, v, prefix, out, out_lse, flop_total)
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    cores_available = len(os.sched_getaffinity(0))
     P, R, Hq, D = w.P, w.R, w.Hq, w.D
     kk = k.cpu().double().numpy()
     vv = v.cpu().double().numpy()
@@ -476,6 +509,8 @@ def cpu_baseline(args, w, plan, rows, q, k, v, prefix, out, out_lse, flop_total)
         "value": round(flop / elapsed / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": int(threads),
+        "cores_available": cores_available,
+        "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": f"{len(done_rows)} of {plan.n_rows} rank-{plan.rank} rows x {Hq} heads over all their "
                   f"visible keys (fp64 numpy), {elapsed:.1f} s",
