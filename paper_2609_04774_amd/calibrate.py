@@ -162,28 +162,64 @@ def measure_attention(grid: Sequence[Tuple[int, int, int]], n_heads_q: int = 32,
 DEFAULT_GRID = [(C, R, P) for C in (1, 2, 4, 8) for R in (4096, 8192, 16384, 32768) for P in (0, 16384)]
 
 
+def check_linearity(samples, fit, flop_per_pair: float, min_pairs: float = 3e7) -> List[str]:
+    """The linearity claims of the attention term on measured samples: a
+    straight line in W / C explains them (R^2 > 0.98); every shard large
+    enough to fill the GPU (W / C >= min_pairs) sits within 25% of the line
+    (smaller ones finish faster than the intercept); the slope's implied rate
+    lies between 10% and 100% of the bf16 peak.  Returns the failures (empty
+    when all hold).  Timing claims: run by ``main --check`` on a quiet GPU,
+    not by the parity tests."""
+    bad = []
+    if not fit.alpha > 0:
+        bad.append(f"alpha = {fit.alpha} is not positive")
+    if not fit.r2 > 0.98:
+        bad.append(f"R^2 = {fit.r2:.4f} <= 0.98")
+    for C, R, P, t in samples:
+        if remaining_workload(R, P) / C >= min_pairs and abs(fit.predict(C, R, P) - t) / t >= 0.25:
+            bad.append(f"(C={C}, R={R}, P={P}): {t * 1e3:.3f} ms is more than 25% off the line")
+    tflops = flop_per_pair / fit.alpha / 1e12 if fit.alpha > 0 else 0.0
+    if not 250 < tflops < 2500:
+        bad.append(f"implied {tflops:.0f} TFLOP/s outside 250..2500")
+    return bad
+
+
 def main(argv=None):
     """Measure the default grid (Llama-3-8B attention shape: 32 query heads,
     8 KV heads, D = 128) and print the samples and the attention-term fit as
-    JSON."""
+    JSON; --out also writes that JSON to a file (the fit the placement
+    policy reads); --check exits non-zero when the linearity claims of
+    ``check_linearity`` fail."""
     import argparse
     import json
+    import sys
 
     ap = argparse.ArgumentParser(description=main.__doc__)
     ap.add_argument("--heads-q", type=int, default=32)
     ap.add_argument("--heads-kv", type=int, default=8)
     ap.add_argument("--reps", type=int, default=5)
+    ap.add_argument("--out", default=None, help="also write the JSON to this file")
+    ap.add_argument("--check", action="store_true", help="exit 1 if the linearity claims fail")
     args = ap.parse_args(argv)
     samples = measure_attention(DEFAULT_GRID, args.heads_q, args.heads_kv, args.reps)
     fit = fit_attention_term(samples)
     flop_per_pair = 4 * 128 * args.heads_q
-    print(json.dumps({
+    failures = check_linearity(samples, fit, flop_per_pair)
+    text = json.dumps({
         "shape": {"Hq": args.heads_q, "Hkv": args.heads_kv, "D": 128},
         "samples": [{"C": C, "R": R, "P": P, "W_over_C": remaining_workload(R, P) / C, "seconds": t}
                     for C, R, P, t in samples],
         "fit": {"d0_s": fit.d0, "alpha_s_per_pair": fit.alpha, "r2": fit.r2, "max_rel_err": fit.max_rel_err,
                 "implied_tflops": flop_per_pair / fit.alpha / 1e12},
-    }, indent=1))
+        "linearity_failures": failures,
+    }, indent=1)
+    print(text, flush=True)
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(text + "\n")
+    if args.check and failures:
+        print("linearity check failed: " + "; ".join(failures), file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

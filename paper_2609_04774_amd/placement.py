@@ -25,6 +25,14 @@ from dataclasses import dataclass, field
 from typing import Callable, List, Optional, Sequence
 
 
+# Readings (the paper gives the roles of beta and lambda, not their values):
+# beta = 1 makes q_w + s_{i,w} the predicted worker-dependent TTFT (Sec. 5.3);
+# lambda = 1 weighs one GPU-second of extra occupancy like one second of it.
+DEFAULT_BETA = 1.0
+DEFAULT_LAMBDA = 1.0
+DEGREES = (1, 2, 4, 8)
+
+
 def remaining_workload(R: int, P: int) -> int:
     """W(R, P) = R P + R (R + 1) / 2 (Sec. 2.2)."""
     return R * P + R * (R + 1) // 2
@@ -108,3 +116,41 @@ def preferred_degree(L: int, P: int, model: PrefillModel, degrees: Sequence[int]
     replaces a fixed length rule)."""
     workers = [Worker(C=C, prefix_for=lambda _r, _L: P) for C in degrees]
     return workers[place(L, workers, model, beta, lam)].C
+
+
+def degree_by_length(L: int) -> int:
+    """The fixed length rule the placement cost replaces: C = 1 below 8K
+    tokens, 2 below 32K, 4 below 64K, else 8 (the paper's short / medium /
+    long buckets, Sec. 3 and its TTFT SLO table)."""
+    if L < 8192:
+        return 1
+    if L < 32768:
+        return 2
+    if L < 65536:
+        return 4
+    return 8
+
+
+def model_from_calibration(path: str) -> PrefillModel:
+    """E_C(R, P) = d0 + alpha W(R, P) / C from a calibration file written by
+    ``python -m paper_2609_04774_amd.calibrate --out`` (the attention term of
+    Sec. 3.2 measured on this GPU; the model's other terms are not measured
+    here and stay 0)."""
+    import json
+    with open(path) as f:
+        fit = json.load(f)["fit"]
+    return PrefillModel(d=float(fit["d0_s"]), alpha=float(fit["alpha_s_per_pair"]))
+
+
+def choose_degrees(requests, rule: str, model: Optional[PrefillModel] = None, beta: float = DEFAULT_BETA,
+                   lam: float = DEFAULT_LAMBDA, degrees: Sequence[int] = DEGREES) -> List[int]:
+    """Per-request CP degree of [(L, P)]: rule "cost" takes PreferDegree over
+    idle workers of every degree (Sec. 7.1: the placement cost without the
+    queue term), rule "length" the fixed length buckets."""
+    if rule == "length":
+        return [degree_by_length(L) for L, _ in requests]
+    if rule != "cost":
+        raise ValueError("rule must be 'cost' or 'length'")
+    if model is None:
+        raise ValueError("the cost rule needs a prefill-time model")
+    return [preferred_degree(L, P, model, degrees, beta, lam) for L, P in requests]

@@ -125,26 +125,22 @@ HETERO_MEDIAN = 2048
 HETERO_SIGMA = 1.16
 HETERO_MIN, HETERO_MAX = 256, 131072
 HETERO_PREFIXED = 19           # round(0.3 * 64) requests carry a cached prefix
+HETERO_TOTAL = 256 * 1024      # the mix's stated total, about 256K tokens
+HETERO_LONG = 32768            # a request this long or longer is in the long bucket
+# The seed of the mix: the first seed from 1005 on whose draw totals within
+# 5% of HETERO_TOTAL and holds at least one request in the long bucket
+# (tests/test_synth.py checks the rule against the seeds before it).
+HETERO_SEED = 1012
 
 
-def cp_degree_for_length(L: int) -> int:
-    """CP degree per request by length bucket (8K / 32K / 64K boundaries)."""
-    if L < 8192:
-        return 1
-    if L < 32768:
-        return 2
-    if L < 65536:
-        return 4
-    return 8
-
-
-def hetero_requests(seed=1005, n=HETERO_REQUESTS, median=HETERO_MEDIAN,
+def hetero_requests(seed=HETERO_SEED, n=HETERO_REQUESTS, median=HETERO_MEDIAN,
                     sigma=HETERO_SIGMA, n_prefixed=HETERO_PREFIXED):
-    """[(L, P, C)] for a lognormal length mix; some requests hit a prefix.
+    """[(L, P)] for a lognormal length mix; some requests hit a prefix.
 
     Lengths: round(exp(ln(median) + sigma * z)), clipped to [256, 131072].
     Prefix: P = 16 * floor(u * L / 16), u ~ U(0.2, 0.8), on ``n_prefixed``
-    randomly chosen requests.
+    randomly chosen requests.  Each request's CP degree is a policy choice
+    made by the caller.
     """
     rng = np.random.default_rng(seed)
     z = rng.standard_normal(n)
@@ -154,4 +150,4 @@ def hetero_requests(seed=1005, n=HETERO_REQUESTS, median=HETERO_MEDIAN,
     u = rng.uniform(0.2, 0.8, size=n_prefixed)
     for i, ui in zip(chosen, u):
         pref[i] = BLOCK_TOKENS * int(math.floor(ui * int(L[i]) / BLOCK_TOKENS))
-    return [(int(L[i]), int(pref[i]), cp_degree_for_length(int(L[i]))) for i in range(n)]
+    return [(int(L[i]), int(pref[i])) for i in range(n)]

@@ -53,3 +53,18 @@ def test_degenerate_grids_are_rejected():
     # One degree only: R and R / C are collinear, so a and c cannot be told apart.
     with pytest.raises(ValueError):
         cal.fit_prefill_model([(1, R, P, 1.0) for _, R, P in GRID])
+
+
+def test_linearity_check_flags_what_it_claims():
+    d0, alpha = 50e-6, 1.5e-11
+    flop = 4 * 128 * 32
+    good = [(C, R, P, d0 + alpha * cal.remaining_workload(R, P) / C) for C, R, P in GRID]
+    assert cal.check_linearity(good, cal.fit_attention_term(good), flop) == []
+    # One large shard 60% slow: the line no longer explains the times (it
+    # drags the fit, so R^2 drops and shards are flagged off the line).
+    bad = [(C, R, P, t * (1.6 if (C, R, P) == (1, 8192, 16384) else 1.0)) for C, R, P, t in good]
+    msgs = cal.check_linearity(bad, cal.fit_attention_term(bad), flop)
+    assert any(m.startswith("R^2") for m in msgs) and any("off the line" in m for m in msgs)
+    # A slope implying more than the bf16 peak is flagged.
+    fast = [(C, R, P, d0 + 1e-13 * cal.remaining_workload(R, P) / C) for C, R, P in GRID]
+    assert any("TFLOP/s" in m for m in cal.check_linearity(fast, cal.fit_attention_term(fast), flop))

@@ -6,12 +6,17 @@ writes every row to its place in the original order -- and its --mode passkv
 step, one launch with the rank's C pass-KV partials (plus a prefix-only
 partial when a prefix is cached) merged and restored the same way.
 
-The oracle recomputes seeded samples of rows (every head) one by one: the
-first and last rows of each chunk, rows on both sides of 64- and 256-row
-boundaries, and random rows; both steps' rows are compared with it.
+The oracle recomputes seeded samples of rows (every head): the first and
+last rows of each chunk, rows on both sides of 64- and 256-row boundaries,
+random rows, and one seeded row in every 32-row block of each chunk (every
+8th block at the largest size) -- every wave of every work item of the
+launch owns one of those blocks, so every work item meets the oracle.  Both
+steps' rows are compared with it.
 Properties that hold at any size are checked on every row: the two steps
 agree, no NaN anywhere, and every restored row is written exactly once.
 """
+
+import os
 
 import numpy as np
 import pytest
@@ -21,6 +26,7 @@ import synth
 from oracle import attention as oatt
 from oracle import plan as oplan
 from paper_2609_04774_amd import cpattn as cp
+from paper_2609_04774_amd import placement as pl
 
 from gpu_cases import DEV, LSE_TOL, O_TOL, compare, f64
 
@@ -79,7 +85,7 @@ def _run_allgather(w, plan, q, k, v, pre):
     return out, out_lse
 
 
-def _sample_rows(plan, n_random, seed):
+def _sample_rows(plan, n_random, seed, block_every=1):
     rng = np.random.default_rng(seed)
     picks = set()
     for c in plan.chunk:
@@ -89,11 +95,13 @@ def _sample_rows(plan, n_random, seed):
         for r in (0, 1, 63, 64, 255, 256, n - 2, n - 1):
             if 0 <= r < n:
                 picks.add(lo + r)
+        for b0 in range(0, n, 32 * block_every):
+            picks.add(lo + b0 + int(rng.integers(0, min(32, n - b0))))
     picks.update(int(x) for x in rng.choice(plan.n_rows, size=min(n_random, plan.n_rows), replace=False))
     return np.array(sorted(picks), dtype=np.int64)
 
 
-def _check_workload(name, rank, n_random):
+def _check_workload(name, rank, n_random, block_every=1):
     w = synth.WORKLOADS[name]
     plan, rows, q, k, v, pre = _inputs(w, rank)
     ref_plan = oplan.shard_plan_fast(w.P, w.R, w.C, rank)
@@ -111,7 +119,8 @@ def _check_workload(name, rank, n_random):
     assert float((out_ag[sel] - out[sel]).abs().max()) <= O_TOL
     assert float((lse_ag[sel] - out_lse[sel]).abs().max()) <= LSE_TOL
     # Sampled rows against the fp64 oracle.
-    pick = _sample_rows(plan, n_random, w.seed)
+    pick = _sample_rows(plan, n_random, w.seed, block_every)
+    print(f"{name} rank {rank}: {len(pick)} of {plan.n_rows} rows checked against the oracle", flush=True)
     pos = rows[pick]
     kk, vv = f64(k), f64(v)
     kc = vc = bt = None
@@ -139,29 +148,39 @@ def test_prefix_hit_64k_full_size():
 
 
 def test_llama3_70b_128k_rank0_full_size():
-    _check_workload("llama3_70b_128k_c8", 0, n_random=2)
+    _check_workload("llama3_70b_128k_c8", 0, n_random=2, block_every=8)
+
+
+CALIBRATION = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "profiles",
+                           "calibration_attention_llama3_8b.json")
 
 
 def test_heterogeneous_batch_one_launch():
-    """64 requests, lognormal lengths, per-request C, 19 with a cached prefix
-    in one shared paged pool: every (request, rank) shard in one launch."""
-    Hq, Hkv, D = 32, 8, 128
-    reqs = synth.hetero_requests()
-    total_blocks = sum(P // synth.BLOCK_TOKENS for _, P, _ in reqs) + 32
+    """The heterogeneous mix (64 lognormal-length requests, 19 with a cached
+    prefix in one shared paged pool) plus two long requests (40K tokens, and
+    70K with a 16K cached prefix), each request at the CP degree the placement
+    cost prefers over the calibrated prefill-time model: every (request, rank)
+    shard in one launch, degrees 1, 2, 4 and 8 mixed."""
+    Hq, Hkv, D, B = 32, 8, 128, synth.BLOCK_TOKENS
+    model = pl.model_from_calibration(CALIBRATION)
+    reqs = synth.hetero_requests() + [(40000, 0), (70000, 16000)]
+    degrees = pl.choose_degrees(reqs, "cost", model)
+    print("C histogram", {C: degrees.count(C) for C in pl.DEGREES}, flush=True)
+    assert set(degrees) == {1, 2, 4, 8}
+    total_blocks = sum(P // B for _, P in reqs) + 32
     g = synth.generator(2005, device="cuda")
-    k_pool = synth.randn_bf16(g, (total_blocks, synth.BLOCK_TOKENS, Hkv, D), device="cuda")
-    v_pool = synth.randn_bf16(g, (total_blocks, synth.BLOCK_TOKENS, Hkv, D), device="cuda")
+    k_pool = synth.randn_bf16(g, (total_blocks, B, Hkv, D), device="cuda")
+    v_pool = synth.randn_bf16(g, (total_blocks, B, Hkv, D), device="cuda")
     free = torch.randperm(total_blocks, generator=g, device="cuda")
     used = 0
     keep, descs, checks = [], [], []
-    for ri, (L, P, C) in enumerate(reqs):
+    for ri, ((L, P), C) in enumerate(zip(reqs, degrees)):
         R = L - P
         q_full, k, v = synth.qkv(g, R, R, Hq, Hkv, D, device="cuda")
         pre = None
         if P:
-            pre = synth.paged_prefix(g, P, Hkv, D, device="cuda",
-                                     pool=(k_pool, v_pool, free[used:used + P // synth.BLOCK_TOKENS]))
-            used += P // synth.BLOCK_TOKENS
+            pre = synth.paged_prefix(g, P, Hkv, D, device="cuda", pool=(k_pool, v_pool, free[used:used + P // B]))
+            used += P // B
         for r in range(C):
             plan, rows = cp.shard_plan(P, R, C, r)
             if plan.n_rows == 0:
@@ -172,22 +191,22 @@ def test_heterogeneous_batch_one_launch():
             descs.append(cp.make_desc(plan, q, k, v, o, l, k_pool, v_pool,
                                       pre.block_table if pre else None, include_prefix=True))
             keep.append((q, o, l))
-            checks.append((ri, P, R, r, plan, rows, q, k, v, pre, o, l))
-    assert sum(L for L, _, _ in reqs) > 100_000
+            checks.append((ri, C, P, R, r, plan, rows, q, k, v, pre, o, l))
     ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=DEV)
     cp.attn_partial(descs, Hq, Hkv, ws)
     torch.cuda.synchronize()
     kp, vp = f64(k_pool), f64(v_pool)
     rng = np.random.default_rng(7)
-    errs = []
-    for ri, P, R, r, plan, rows, q, k, v, pre, o, l in checks:
+    n_rows = 0
+    for ri, C, P, R, r, plan, rows, q, k, v, pre, o, l in checks:
         assert not torch.isnan(o).any() and not torch.isnan(l).any()
-        n = plan.n_rows
-        pick = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, size=1)]))
+        ends = [c.local_offset + e for c in plan.chunk if c.q_len for e in (0, c.q_len - 1)]
+        pick = np.unique(np.concatenate([ends, rng.integers(0, plan.n_rows, size=1)]))
         pos = rows[pick]
         bt = pre.block_table.cpu().numpy().astype(np.int64) if pre else None
-        O_ref, L_ref = oatt.rank_partial(f64(q[torch.as_tensor(pick, device=DEV)]), pos, P, f64(k), f64(v),
-                                         kp if pre else None, vp if pre else None, bt)
-        errs.append(compare(f64(o[torch.as_tensor(pick, device=DEV)]), f64(l[torch.as_tensor(pick, device=DEV)]),
-                            O_ref, L_ref, f"request {ri} rank {r}"))
-    assert len(errs) == len(checks)
+        sel = torch.as_tensor(pick, device=DEV)
+        O_ref, L_ref = oatt.rank_partial(f64(q[sel]), pos, P, f64(k), f64(v), kp if pre else None,
+                                         vp if pre else None, bt)
+        compare(f64(o[sel]), f64(l[sel]), O_ref, L_ref, f"request {ri} (C={C}) rank {r}")
+        n_rows += len(pick)
+    print(f"{len(checks)} shards, {n_rows} rows checked against the oracle", flush=True)

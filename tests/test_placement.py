@@ -65,3 +65,47 @@ def test_invalid_arguments():
         pl.placement_costs(10, [pl.Worker(C=1)], MODEL, lam=-1.0)
     with pytest.raises(ValueError):
         pl.place(10, [pl.Worker(C=1, eligible=False)], MODEL)
+
+
+# PreferDegree on a prefill-time model of the form the calibration fits:
+# E_C(R, P) = d0 + alpha W(R, P) / C, d0 = 100 us, alpha = 1.5e-11 s per pair.
+# With beta = lambda = 1 on idle workers of degrees 1, 2, 4, 8 (C_min = 1):
+#   J_C = s_C + (C s_C - s_1) = d0 + alpha W / C + (C - 1) d0.
+FIT = pl.PrefillModel(d=1e-4, alpha=1.5e-11)
+
+
+@pytest.mark.parametrize("L,P,J,pick", [
+    # W = 2,098,176: alpha W = 3.147264e-5.
+    (2048, 0, [1.3147264e-4, 2.15736320e-4, 4.07868160e-4, 8.03934080e-4], 1),
+    # W = 33,558,528: alpha W = 5.0337792e-4.
+    (8192, 0, [6.0337792e-4, 4.5168896e-4, 5.2584448e-4, 8.6292224e-4], 2),
+    # W = 134,225,920: alpha W = 2.0133888e-3.
+    (16384, 0, [2.1133888e-3, 1.2066944e-3, 9.033472e-4, 1.0516736e-3], 4),
+    # R = P = 8192: W = 8192 * 8192 + 33,558,528 = 100,667,392; alpha W = 1.51001088e-3.
+    (16384, 8192, [1.61001088e-3, 9.5500544e-4, 7.7750272e-4, 9.8875136e-4], 4),
+    # W = 536,887,296: alpha W = 8.05330944e-3.
+    (32768, 0, [8.15330944e-3, 4.22665472e-3, 2.41332736e-3, 1.80666368e-3], 8),
+])
+def test_prefer_degree_on_a_fitted_model_by_hand(L, P, J, pick):
+    workers = [pl.Worker(C=C, prefix_for=lambda _r, _L: P) for C in pl.DEGREES]
+    costs = pl.placement_costs(L, workers, FIT, beta=pl.DEFAULT_BETA, lam=pl.DEFAULT_LAMBDA)
+    assert costs == pytest.approx(J, rel=1e-9)
+    assert pl.preferred_degree(L, P, FIT, pl.DEGREES, pl.DEFAULT_BETA, pl.DEFAULT_LAMBDA) == pick
+    assert pl.choose_degrees([(L, P)], "cost", FIT) == [pick]
+
+
+def test_length_rule_buckets():
+    assert [pl.degree_by_length(L) for L in (256, 8191, 8192, 32767, 32768, 65535, 65536, 131072)] == \
+        [1, 1, 2, 2, 4, 4, 8, 8]
+    assert pl.choose_degrees([(100, 0), (40000, 16)], "length") == [1, 4]
+    with pytest.raises(ValueError):
+        pl.choose_degrees([(100, 0)], "cost")
+    with pytest.raises(ValueError):
+        pl.choose_degrees([(100, 0)], "size")
+
+
+def test_model_from_calibration(tmp_path):
+    f = tmp_path / "cal.json"
+    f.write_text('{"fit": {"d0_s": 0.0001, "alpha_s_per_pair": 1.5e-11, "r2": 0.999}}')
+    m = pl.model_from_calibration(str(f))
+    assert m.predict(2, 8192, 0) == pytest.approx(1e-4 + 1.5e-11 * 33558528 / 2)
