@@ -304,10 +304,15 @@ def main():
     value = flop / (ms_step * 1e-3) / 1e12
 
     def timed(fn, reps=10):
+        """GPU time per call of fn (its launches back to back).  A GPU-side
+        wait is queued first, so that every repetition is enqueued before the
+        GPU reaches them: for launches shorter than the binding's own host
+        time the events then bracket the kernels, not the host's call rate."""
         fn()
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(5_000_000)
         a.record(stream)
         for _ in range(reps):
             fn()
