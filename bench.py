@@ -5,12 +5,13 @@ A step is one pass of the whole path for rank 0 of the workload:
   1. the zigzag shard plan (host, cp_shard_plan);
   2. partial attention of the rank's rows -- one cp_attn_partial launch:
      by default (--mode allgather) against every key the rank's rows see in
-     the all-gathered KV (and the paged prefix, if any), one descriptor;
+     the all-gathered KV (and the paged prefix, if any), one descriptor whose
+     output rows are stored at their places in the original sequence order
+     (CP_OUT_SEQUENCE: the restore done by the attention's own stores);
      with --mode passkv against each of the C ranks' KV shards (and the
-     prefix) separately, C (+1) descriptors;
-  3. cp_attn_merge with the plan: the exact LSE merge of the partials (one
-     partial in the all-gather view), writing each row back to its place in
-     the original sequence order.
+     prefix) separately, C (+1) descriptors in local row order;
+  3. --mode passkv only: cp_attn_merge with the plan, the exact LSE merge of
+     the partials, writing each row back to its place in sequence order.
 Inputs are resident in HBM before the timed region starts.  In the
 all-gather view the merge object reports a separate leg: C (+1) partials of
 the same rows (seeded values, every LSE finite, so every partial is read)
@@ -235,10 +236,11 @@ def main():
     else:
         shard_ids = [cp.CP_KV_ALL]
         n_parts = 1
-    o_parts = torch.empty((n_parts, n_rows, Hq, D), dtype=torch.float32, device=dev)
-    l_parts = torch.empty((n_parts, n_rows, Hq), dtype=torch.float32, device=dev)
     out = torch.empty((R, Hq, D), dtype=torch.float32, device=dev)
     out_lse = torch.empty((R, Hq), dtype=torch.float32, device=dev)
+    if args.mode == "passkv":
+        o_parts = torch.empty((n_parts, n_rows, Hq, D), dtype=torch.float32, device=dev)
+        l_parts = torch.empty((n_parts, n_rows, Hq), dtype=torch.float32, device=dev)
 
     def make_descs(pl):
         descs = []
@@ -247,9 +249,12 @@ def main():
             descs.append(cp.make_desc(pl, q, k, v, o_parts[i], l_parts[i], kc, vc, bt,
                                       include_prefix=True, kv_rank=cp.CP_KV_NONE))
             i += 1
+        if args.mode == "allgather":
+            return [cp.make_desc(pl, q, k, v, out, out_lse, kc, vc, bt, include_prefix=True,
+                                 kv_rank=cp.CP_KV_ALL, out_order=cp.CP_OUT_SEQUENCE)]
         for s in shard_ids:
             descs.append(cp.make_desc(pl, q, k, v, o_parts[i], l_parts[i], kc, vc, bt,
-                                      include_prefix=(args.mode == "allgather"), kv_rank=s))
+                                      include_prefix=False, kv_rank=s))
             i += 1
         return descs
 
@@ -281,8 +286,9 @@ def main():
         cp.attn_partial(descs, Hq, Hkv, ws, stream=stream)
         if record:
             e1.record(stream)
-        cp.attn_merge([o_parts[i] for i in range(n_parts)], [l_parts[i] for i in range(n_parts)],
-                      out, out_lse, restore=pl, stream=stream)
+        if args.mode == "passkv":
+            cp.attn_merge([o_parts[i] for i in range(n_parts)], [l_parts[i] for i in range(n_parts)],
+                          out, out_lse, restore=pl, stream=stream)
         if record:
             e2.record(stream)
             ev.append((e0, e1, e2))
@@ -409,7 +415,7 @@ def main():
             "workload": w.name, "L": w.L, "P": P, "R": R, "C": C, "rank": rank, "Hq": Hq,
             "Hkv": Hkv, "D": D, "rows": n_rows, "visible_pairs_per_head": plan.visible_pairs,
             "flop_per_step": flop, "mode": ("pass-KV partials + LSE merge + restore" if args.mode == "passkv"
-                                            else "all-gathered KV partial + restore"),
+                                            else "all-gathered KV partial stored in sequence order"),
             "partials": n_parts,
         },
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),

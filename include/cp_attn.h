@@ -71,6 +71,10 @@ extern "C" {
 #define CP_KV_ALL (-1)  /* every causally visible suffix key (all-gathered KV) */
 #define CP_KV_NONE (-2) /* no suffix key (prefix-only partial) */
 
+/* Row order of a partial's outputs (cp_partial_desc.out_order). */
+#define CP_OUT_LOCAL 0    /* the rank's rows in local order, as its queries */
+#define CP_OUT_SEQUENCE 1 /* rows at their suffix index in an R-row output */
+
 /* Static description of a status code.  (Library utility; not from the
  * paper.) */
 const char* cp_status_string(int status);
@@ -152,10 +156,18 @@ int cp_shard_inverse(int64_t prefix_len, int64_t new_len, int32_t C,
  *               (the paper's all-gathered CP); r in 0..C-1: only to the suffix
  *               keys of rank r's two zigzag chunks (pass-KV partial; the C
  *               shards partition the suffix); CP_KV_NONE: to no suffix key.
- *   o           fp32 [plan.n_rows][Hq][D], normalised partial output.
- *   lse         fp32 [plan.n_rows][Hq], natural-log LSE (-inf: no key).
+ *   o           fp32 [rows][Hq][D], normalised partial output.
+ *   lse         fp32 [rows][Hq], natural-log LSE (-inf: no key).
  *   n_blocks    blocks in k_cache and v_cache; >= 1 when the prefix is read.
  *               Values above 2^31 - 1 act as 2^31 - 1 (entries are int32).
+ *   out_order   CP_OUT_LOCAL: o and lse have rows = plan.n_rows, the rank's
+ *               rows in local order.  CP_OUT_SEQUENCE: o and lse have rows =
+ *               R in the original suffix order (row i = position P + i) and
+ *               the call writes only this rank's rows there -- the restore of
+ *               Sec. 2.1 done by the attention's own stores, so a rank's one
+ *               all-gathered partial needs no cp_attn_merge.  Other values:
+ *               CP_ERR_INVALID.
+ *   reserved    must be 0.
  * Merging (cp_attn_merge) the C pass-KV partials plus a prefix-only partial
  * gives the CP_KV_ALL result with include_prefix = 1.
  */
@@ -172,6 +184,8 @@ typedef struct cp_partial_desc {
   float* o;
   float* lse;
   int64_t n_blocks;
+  int32_t out_order;
+  int32_t reserved;
 } cp_partial_desc;
 
 /*

@@ -27,6 +27,8 @@ CP_KV_BLOCK_TOKENS = 16
 CP_MAX_MERGE_PARTS = 16
 CP_KV_ALL = -1
 CP_KV_NONE = -2
+CP_OUT_LOCAL = 0
+CP_OUT_SEQUENCE = 1
 CP_MAX_DEGREE = 64
 CP_NOALLOC_SCRATCH_BYTES = 32 << 20
 
@@ -65,7 +67,8 @@ class CpPartialDesc(ctypes.Structure):
                 ("block_table", ctypes.c_void_p),
                 ("include_prefix", ctypes.c_int32), ("kv_rank", ctypes.c_int32),
                 ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p),
-                ("n_blocks", ctypes.c_int64)]
+                ("n_blocks", ctypes.c_int64),
+                ("out_order", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class CpError(RuntimeError):
@@ -198,16 +201,22 @@ def _dev(t, name: str, dtype=None, rows: Optional[int] = None, tail=None):
 
 
 def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=None,
-              block_table=None, include_prefix: bool = True, kv_rank: int = CP_KV_ALL) -> CpPartialDesc:
+              block_table=None, include_prefix: bool = True, kv_rank: int = CP_KV_ALL,
+              out_order: int = CP_OUT_LOCAL) -> CpPartialDesc:
     """A cp_partial_desc over torch device tensors (layouts in include/cp_attn.h).
-    The tensors' head counts are checked against n_heads_q / n_heads_kv when
-    the descriptor is launched.  The descriptor keeps references to its
-    tensors; keep it until the launch has been issued."""
+    With out_order=CP_OUT_SEQUENCE, o and lse have R rows in the original
+    suffix order and only this rank's rows are written.  The tensors' head
+    counts are checked against n_heads_q / n_heads_kv when the descriptor is
+    launched.  The descriptor keeps references to its tensors; keep it until
+    the launch has been issued."""
     import torch
     D = CP_HEAD_DIM
+    if out_order not in (CP_OUT_LOCAL, CP_OUT_SEQUENCE):
+        raise ValueError("out_order must be CP_OUT_LOCAL or CP_OUT_SEQUENCE")
+    out_rows = plan.new_len if out_order == CP_OUT_SEQUENCE else plan.n_rows
     _dev(q, "q", torch.bfloat16, plan.n_rows)
-    _dev(o, "o", torch.float32, plan.n_rows)
-    _dev(lse, "lse", torch.float32, plan.n_rows)
+    _dev(o, "o", torch.float32, out_rows)
+    _dev(lse, "lse", torch.float32, out_rows)
     _dev(k_new, "k_new", torch.bfloat16, plan.new_len)
     _dev(v_new, "v_new", torch.bfloat16, plan.new_len)
     _dev(k_cache, "k_cache", torch.bfloat16)
@@ -237,6 +246,8 @@ def make_desc(plan: CpRankPlan, q, k_new, v_new, o, lse, k_cache=None, v_cache=N
     d.o = _ptr(o)
     d.lse = _ptr(lse)
     d.n_blocks = k_cache.shape[0] if k_cache is not None else 0
+    d.out_order = out_order
+    d.reserved = 0
     d._heads = (q, o, lse, k_new, v_new, k_cache, v_cache)
     # The descriptor holds only device pointers: keep every tensor it points
     # at alive for as long as the descriptor exists, so that a caller that

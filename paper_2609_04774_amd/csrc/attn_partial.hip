@@ -534,7 +534,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // Positions are below 2^30 (checked on the host): 32 bits suffice.
   const int q_begin = (int)(it.chunk ? d.q_begin[1] : d.q_begin[0]);
   const int q_len = (int)(it.chunk ? d.q_len[1] : d.q_len[0]);
-  const int64_t loff = it.chunk ? d.local_off[1] : d.local_off[0];
+  const int64_t loff = it.chunk ? d.local_off[1] : d.local_off[0];  // Q row of the chunk's first query
+  const int64_t ooff = it.chunk ? d.o_off[1] : d.o_off[0];          // its O / LSE row
   const int Hq = p.Hq;
   const int Hkv = p.Hkv;
   const int kvh = it.head_group / p.groups_per_kv;
@@ -593,7 +594,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
 #pragma unroll
     for (int b = 0; b < kNB; ++b) {
       if (!valid_b[b]) continue;
-      const int64_t row = loff + qb0 + qrel_b[b];
+      const int64_t row = ooff + qb0 + qrel_b[b];
       float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
 #pragma unroll
       for (int c = 0; c < kHeadDim / 8; ++c)
@@ -851,7 +852,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       if (half == 0)
         reinterpret_cast<float*>(slot + kPieceOBytes)[r] = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
     } else if (valid_b[b]) {
-      const int64_t row = loff + qb0 + qrel_b[b];
+      const int64_t row = ooff + qb0 + qrel_b[b];
       float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
 #pragma unroll
       for (int db = 0; db < 4; ++db)
@@ -893,7 +894,7 @@ __global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restr
   const int64_t qb0 = (int64_t)sp.q_block * p.q_per_wg;
   const int64_t q_len = sp.chunk ? d.q_len[1] : d.q_len[0];
   if (qb0 + qrel >= q_len) return;
-  const int64_t row = (sp.chunk ? d.local_off[1] : d.local_off[0]) + qb0 + qrel;
+  const int64_t row = (sp.chunk ? d.o_off[1] : d.o_off[0]) + qb0 + qrel;
 
   float m = -INFINITY;
   for (int k = 0; k < sp.n_pieces; ++k) {

@@ -77,6 +77,9 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
   if (P + R > ((int64_t)1 << 30)) return fail(CP_ERR_UNSUPPORTED, who + "sequence beyond 2^30 tokens");
   if (x.kv_rank < CP_KV_NONE || x.kv_rank >= pl.C) return fail(CP_ERR_INVALID, who + "kv_rank out of range");
   if (x.include_prefix != 0 && x.include_prefix != 1) return fail(CP_ERR_INVALID, who + "include_prefix must be 0 or 1");
+  if (x.out_order != CP_OUT_LOCAL && x.out_order != CP_OUT_SEQUENCE)
+    return fail(CP_ERR_INVALID, who + "out_order must be CP_OUT_LOCAL or CP_OUT_SEQUENCE");
+  if (x.reserved != 0) return fail(CP_ERR_INVALID, who + "reserved must be 0");
   if (pl.n_rows > 0) {
     if (!x.q || !x.o || !x.lse) return fail(CP_ERR_INVALID, who + "q, o and lse are required");
     if (!aligned(x.q, 16) || !aligned(x.o, 16) || !aligned(x.lse, 4))
@@ -114,6 +117,8 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
     d.q_begin[i] = pl.chunk[i].q_begin;
     d.q_len[i] = pl.chunk[i].q_len;
     d.local_off[i] = pl.chunk[i].local_offset;
+    // Sequence order: the chunk's first query is suffix index q_begin - P.
+    d.o_off[i] = x.out_order == CP_OUT_SEQUENCE ? pl.chunk[i].q_begin - P : pl.chunk[i].local_offset;
   }
   d.prefix_keys = use_prefix ? (int32_t)P : 0;
   // Entries are int32: a cache of more blocks than that holds every entry.

@@ -63,7 +63,8 @@ struct DevDesc {
   int64_t R;
   int64_t q_begin[2];
   int64_t q_len[2];
-  int64_t local_off[2];
+  int64_t local_off[2];  // Q row of each chunk's first query
+  int64_t o_off[2];      // O / LSE row of each chunk's first query
   int64_t seg_lo[2];
   int64_t seg_hi[2];
   int32_t n_seg;

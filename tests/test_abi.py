@@ -74,7 +74,7 @@ def test_struct_layout_matches_header():
     # 4+4 + 5*8 + 2*(4+4+3*8) + 8 bytes
     assert ctypes.sizeof(cp.CpChunk) == 32
     assert ctypes.sizeof(cp.CpRankPlan) == 8 + 5 * 8 + 2 * 32 + 8
-    assert ctypes.sizeof(cp.CpPartialDesc) == ctypes.sizeof(cp.CpRankPlan) + 6 * 8 + 8 + 2 * 8 + 8
+    assert ctypes.sizeof(cp.CpPartialDesc) == ctypes.sizeof(cp.CpRankPlan) + 6 * 8 + 8 + 2 * 8 + 8 + 8
 
 
 PLAN_SWEEP = [(P, R, C) for P in (0, 16, 48, 49152) for R in (0, 1, 3, 7, 16, 100, 1024, 1000)
@@ -198,6 +198,8 @@ def _desc(P=0, R=64, C=2, rank=0, **kw):
     d.o = kw.get("o", FAKE * 7)
     d.lse = kw.get("lse", FAKE * 8)
     d.n_blocks = kw.get("n_blocks", 8)
+    d.out_order = kw.get("out_order", cp.CP_OUT_LOCAL)
+    d.reserved = kw.get("reserved", 0)
     return d
 
 
@@ -221,6 +223,9 @@ def _partial_status(descs, Hq=8, Hkv=2, D=128, ws=FAKE * 16, ws_bytes=1 << 30):
     ("misaligned q", {"q": FAKE + 2}, {}, cp.CP_ERR_INVALID),
     ("misaligned k_cache", {"P": 32, "k_cache": FAKE + 8}, {}, cp.CP_ERR_INVALID),
     ("include_prefix 2", {"include_prefix": 2}, {}, cp.CP_ERR_INVALID),
+    ("out_order 2", {"out_order": 2}, {}, cp.CP_ERR_INVALID),
+    ("out_order -1", {"out_order": -1}, {}, cp.CP_ERR_INVALID),
+    ("reserved not 0", {"reserved": 1}, {}, cp.CP_ERR_INVALID),
     ("workspace too small", {}, {"ws_bytes": 16}, cp.CP_ERR_CAPACITY),
     ("workspace null", {}, {"ws": None}, cp.CP_ERR_INVALID),
     ("workspace misaligned", {}, {"ws": FAKE + 64}, cp.CP_ERR_INVALID),
@@ -435,3 +440,19 @@ def test_repartition_all_argument_errors():
     assert "set 1 rank 3" in cp.last_error()
     # R < 2C: ranks without rows may be NULL; R = 0 launches nothing.
     assert _rpa_status(R=0, src=[None] * 4, dst=[None] * 8) == cp.CP_OK
+
+
+def test_binding_constants_match_the_header():
+    """Every #define of include/cp_attn.h that the binding mirrors has the
+    header's value."""
+    import re
+    hdr = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                            "cp_attn.h")).read()
+    found = 0
+    for name, val in re.findall(r"^#define (CP_[A-Z0-9_]+) +\(?(-?\d+)\)?(?: |$)", hdr, re.M):
+        if hasattr(cp, name):
+            assert getattr(cp, name) == int(val), name
+            found += 1
+    assert found >= 14
+    assert cp.CP_NOALLOC_SCRATCH_BYTES == 32 << 20  # (32u << 20) in the header
+    assert cp.CP_OUT_LOCAL == 0 and cp.CP_OUT_SEQUENCE == 1

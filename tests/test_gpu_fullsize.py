@@ -1,10 +1,10 @@
 """GPU parity at the full workload sizes, in both launch configurations that
 bench.py times: its default step -- one cp_attn_partial launch of the rank's
 rows against every key they see in the all-gathered KV (and the paged
-prefix), then cp_attn_merge of that one partial with the rank's plan, which
-writes every row to its place in the original order -- and its --mode passkv
-step, one launch with the rank's C pass-KV partials (plus a prefix-only
-partial when a prefix is cached) merged and restored the same way.
+prefix), whose stores put every row at its place in the original order
+(CP_OUT_SEQUENCE) -- and its --mode passkv step, one launch with the rank's C
+pass-KV partials (plus a prefix-only partial when a prefix is cached), merged
+and restored by cp_attn_merge with the rank's plan.
 
 The oracle recomputes seeded samples of rows (every head): the first and
 last rows of each chunk, rows on both sides of 64- and 256-row boundaries,
@@ -70,17 +70,15 @@ def _run_passkv(w, plan, q, k, v, pre):
 
 
 def _run_allgather(w, plan, q, k, v, pre):
-    """bench.py's default step: one partial over all visible keys, restored
-    by the merge of that one partial."""
-    o = torch.empty((plan.n_rows, w.Hq, w.D), dtype=torch.float32, device=DEV)
-    l = torch.empty((plan.n_rows, w.Hq), dtype=torch.float32, device=DEV)
+    """bench.py's default step: one partial over all visible keys, its rows
+    stored straight into their places in sequence order."""
     kc, vc, bt = (pre.k_cache, pre.v_cache, pre.block_table) if pre else (None, None, None)
-    d = cp.make_desc(plan, q, k, v, o, l, kc, vc, bt, include_prefix=True, kv_rank=cp.CP_KV_ALL)
-    ws = torch.empty(max(256, cp.workspace_size([d], w.Hq, w.Hkv)), dtype=torch.uint8, device=DEV)
-    cp.attn_partial([d], w.Hq, w.Hkv, ws)
     out = torch.full((w.R, w.Hq, w.D), float("nan"), dtype=torch.float32, device=DEV)
     out_lse = torch.full((w.R, w.Hq), float("nan"), dtype=torch.float32, device=DEV)
-    cp.attn_merge([o], [l], out, out_lse, restore=plan)
+    d = cp.make_desc(plan, q, k, v, out, out_lse, kc, vc, bt, include_prefix=True, kv_rank=cp.CP_KV_ALL,
+                     out_order=cp.CP_OUT_SEQUENCE)
+    ws = torch.empty(max(256, cp.workspace_size([d], w.Hq, w.Hkv)), dtype=torch.uint8, device=DEV)
+    cp.attn_partial([d], w.Hq, w.Hkv, ws)
     torch.cuda.synchronize()
     return out, out_lse
 

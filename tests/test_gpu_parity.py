@@ -122,6 +122,42 @@ def test_pass_kv_and_prefix_only_partials(L, P, C, Hq, Hkv, seed):
             compare(f64(o), f64(lse), Or, Lr, f"rank {r} prefix only")
 
 
+# out_order = CP_OUT_SEQUENCE: each rank's rows are stored at their suffix
+# index of one R-row output by the attention itself (the restore of Sec. 2.1,
+# no merge).  (8392, 8192) splits its key walks, so the split-merge kernel's
+# stores are covered too.
+@pytest.mark.parametrize("L,P,C,Hq,Hkv,seed", [(1000, 0, 2, 8, 2, 81), (777, 0, 4, 4, 4, 82),
+                                                (640, 80, 3, 16, 1, 83), (8392, 8192, 2, 8, 2, 84),
+                                                (5, 0, 4, 8, 1, 85)])
+def test_sequence_order_output(L, P, C, Hq, Hkv, seed):
+    prob = Problem(L, P, C, Hq, Hkv, seed)
+    dv, R = prob.dev(), prob.R
+    O, LSE = gc.alloc_out(R, Hq)
+    O2, LSE2 = gc.alloc_out(R, Hq)
+    together = []
+    for r in range(C):
+        plan, rows = cp.shard_plan(P, R, C, r)
+        if plan.n_rows == 0:
+            continue
+        q = dv["q"][torch.as_tensor(rows - P, device=DEV)].contiguous()
+        # One launch per rank, as its local-order launch: the same work
+        # decomposition, so the stored rows must be the same bits.
+        d = cp.make_desc(plan, q, dv["k"], dv["v"], O, LSE, dv.get("kc"), dv.get("vc"), dv.get("bt"),
+                         out_order=cp.CP_OUT_SEQUENCE)
+        gc.run_partials([d], Hq, Hkv)
+        o, lse, _, _ = prob.gpu_rank(r)
+        at = torch.as_tensor(rows - P, device=DEV)
+        assert torch.equal(O[at], o) and torch.equal(LSE[at], lse), f"rank {r}"
+        together.append(cp.make_desc(plan, q, dv["k"], dv["v"], O2, LSE2, dv.get("kc"), dv.get("vc"),
+                                     dv.get("bt"), out_order=cp.CP_OUT_SEQUENCE))
+    # Every rank in one launch, into one output: every row written once, and
+    # the whole output is single-rank causal attention (Sec. 2.1).
+    gc.run_partials(together, Hq, Hkv)
+    Or, Lr = _oracle_full(prob)
+    compare(f64(O[:R]), f64(LSE[:R]), Or, Lr, "per-rank launches")
+    compare(f64(O2[:R]), f64(LSE2[:R]), Or, Lr, "one launch")
+
+
 # Launches with few work items, so the key walks are split into pieces of
 # >= 32 tiles whose partials are merged in the workspace: a long cached
 # prefix under a short suffix (the prefix-hit case), and a small-head shard
