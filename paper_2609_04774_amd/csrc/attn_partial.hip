@@ -48,6 +48,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -329,7 +330,7 @@ __device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffse
 
 // O^T += V^T P^T for one 32-key tile (the last one).
 __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
-                                        f32x16 (&o)[4][kNB]) {
+                                        f32x16 (&o)[4][kNB], const bf16x8& sel, f32x4& psum) {
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
@@ -338,6 +339,7 @@ __device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffse
 #pragma unroll
       for (int b = 0; b < kNB; ++b) o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
     }
+    psum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[0][ks], psum, 0, 0, 0);
   }
 }
 
@@ -405,26 +407,23 @@ __device__ __forceinline__ void pin(const T& x) {
 
 struct SoftmaxState {
   float rs;       // fp32 sum of this tile's probabilities
-  float rsb;      // sum of the bf16-rounded probabilities
   bf16x2 pp[8];
 };
 
-constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
-
 // Pair t of the tile's 16 scores (registers 2t, 2t+1, already
-// exponentiated): rounded to bf16 once, and added to both sums.
+// exponentiated): rounded to bf16 once (the P operand of O += V P), and
+// added to the tile's fp32 sum (the LSE's).  The sum of the bf16-rounded
+// values, which normalises O, is taken by an MFMA over the P fragments
+// (psum in the kernel): a dot-product instruction here would share the
+// matrix pipes with the tile's MFMAs and cost far more issue time.
 __device__ __forceinline__ void pack_and_sum(int t, const f32x16& s, SoftmaxState& st) {
   const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
   st.pp[t] = pp;
-  if (t == 0) {
+  if (t == 0)
     st.rs = s[0] + s[1];
-    st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, 0.f, false);
-  } else {
+  else
     st.rs += s[2 * t] + s[2 * t + 1];
-    st.rsb = __builtin_amdgcn_fdot2_f32_bf16(pp, kOnes, st.rsb, false);
-  }
   pin(st.rs);
-  pin(st.rsb);
   pin(pp);
 }
 
@@ -465,7 +464,7 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
                                                  const bf16x8 (&qf)[kNB][8], const bf16x8 (&pf)[kNB][2],
                                                  f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB],
                                                  float m_run, float sl2, const TileLoad& ld, SoftmaxState& st,
-                                                 bf16x8 (&pre)[kLookahead]) {
+                                                 bf16x8 (&pre)[kLookahead], const bf16x8& sel, f32x4& psum) {
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = pre[g];
@@ -479,6 +478,8 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
     if ((slot & 7) == 1) issue_load(ld, slot >> 3);
     if (slot < 8) {
       o[slot & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][slot >> 2], o[slot & 3][0], 0, 0, 0);
+      // After a k-step's last P V product: the bf16 row sums of its 16 keys.
+      if ((slot & 3) == 3) psum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[0][slot >> 2], psum, 0, 0, 0);
     } else {
       mfma_qk(s_out[0], fr[slot], qf[0][slot - 8], slot == 8);
     }
@@ -493,12 +494,12 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
 // where that is higher, O and the running sums are rescaled by 2^(m_old -
 // m_new) (exactly 1 where it did not move, 0 before a query's first visible
 // key), and the tile's probabilities are taken against the new max.
-__device__ __forceinline__ void exact_softmax(f32x16& s, float& m_run, float& l_run, float& lb_run,
+__device__ __forceinline__ void exact_softmax(f32x16& s, float& m_run, float& l_run, f32x4& psum,
                                               f32x16 (&o)[4][kNB], float sl2, SoftmaxState& st) {
   const float m_new = __builtin_elementwise_maximum(tile_max(s, sl2), m_run);
   const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
   l_run *= alpha;
-  lb_run *= alpha;
+  psum *= alpha;
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db][0] *= alpha;
   m_run = m_new;
@@ -702,7 +703,21 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const float sl2 = p.scale_log2;
   f32x16 o[4][kNB];
   float m_run[kNB];                            // running max (exponent units)
-  float l_run[kNB], lb_run[kNB];               // sums of the fp32 / bf16-rounded probabilities (lane's keys)
+  float l_run[kNB];                            // sum of the fp32 probabilities (lane's keys)
+  // Sums of the bf16-rounded probabilities, by a 16x16x32 MFMA over the P
+  // fragments: with the P^T fragment read as its B operand, lane l holds
+  // query 16 * ((l / 16) % 2) + l % 16's keys of k-group l / 16 (k = 8 * (l /
+  // 16) + j), so a selector A with A[m][k] = 1 iff (k / 8) % 2 == m % 2 sums
+  // every key of query n (even m) and of query 16 + n (odd m) into C[m][n].
+  // Lane l holds C[4 * (l / 16) + r][l % 16]: r = 0 for query l % 16, r = 1
+  // for query 16 + l % 16.
+  f32x4 psum = f32x4{};
+  bf16x8 sel;
+  {
+    const __bf16 one = (((lane >> 4) & 1) == ((lane & 15) & 1)) ? (__bf16)1.0f : (__bf16)0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sel[e] = one;
+  }
   bf16x8 pf[kNB][2];                           // P of the previous tile
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
@@ -710,7 +725,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
     m_run[b] = kNoMax;
     l_run[b] = 0.f;
-    lb_run[b] = 0.f;
     pf[b][0] = pf[b][1] = bf16x8{};
   }
   // Scores of the current tile alternate between two register sets.
@@ -777,17 +791,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     const TileLoad ld = next_load(j);
     SoftmaxState st;
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes,
-                     smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run[0], sl2, ld, st, pre);
+                     smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run[0], sl2, ld, st, pre, sel, psum);
     // Rare: some lane's probabilities were too large (its max grew by more
     // than ~2^12, or it saw its first key).  Redo the tile exactly; its K
     // tile is still in buffer B (tile j + 8 is loaded three iterations on).
     if (__builtin_amdgcn_ballot_w64(!(st.rs <= kMaxTileSum)) != 0) {
       qk_tile(smem + B * kTileBytes, fo, qf, s_in);
       mask_if_needed(j, s_in);
-      exact_softmax(s_in[0], m_run[0], l_run[0], lb_run[0], o, sl2, st);
+      exact_softmax(s_in[0], m_run[0], l_run[0], psum, o, sl2, st);
     }
     l_run[0] += st.rs;
-    lb_run[0] += st.rsb;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
       pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
@@ -822,14 +835,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0 && wave_active) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o);
+  if (n_tiles > 0 && wave_active) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, sel, psum);
 
   // Normalise and store: O^T register r of d-block db is head-dim
   // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
     const float lt = xsum32(l_run[b]);
-    const float ltb = xsum32(lb_run[b]);
+    const float ltb = ((lane >> 4) & 1) ? psum[1] : psum[0];
     const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
     const float inv = live ? 1.f / ltb : 0.f;
     if (it.piece >= 0) {
