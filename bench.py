@@ -41,6 +41,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+NOMINAL_CLOCK_GHZ = 2.4        # the clock the bf16 peak is quoted at
 METRIC = "CP-shard causal prefill attention TFLOP/s + % bf16 MFMA peak; merge GB/s"
 DEFAULT_WORKLOAD = "llama3_8b_32k_c4"
 
@@ -183,15 +184,19 @@ def heterogeneous_batch(args, gen, dev, stream, reps=5):
     return out
 
 
-def counter_profile(workload, args, rank):
+def counter_profile(workload, args, rank, frac):
     """The committed counter profile's clock and MFMA-busy fraction for this
-    launch configuration (null when there is none for the current source)."""
+    launch configuration (null when there is none for the current source),
+    and this run's fraction of peak re-based to that sustained clock: the
+    peak the matrix cores can reach at the clock the chip holds under this
+    load (2.5 PFLOP/s x clock / 2.4 GHz)."""
     if rank != 0:
         return None
     f = profiled_figures(workload, args.mode)
     if f is None or "clock_ghz" not in f:
         return None
     return {"clock_ghz": f["clock_ghz"], "mfma_busy": f["mfma_busy"],
+            "frac_at_profiled_clock": round(frac * NOMINAL_CLOCK_GHZ / f["clock_ghz"], 4),
             "source": f"profiles/traffic_{workload}_{args.mode}.txt "
                       "(rocprofv3 GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES)"}
 
@@ -428,7 +433,7 @@ def main():
             "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": measured_traffic(w.name, args.mode) if rank == 0 else None,
             "launch_ms": round(attn_ms, 4),
-            "profiled": counter_profile(w.name, args, rank),
+            "profiled": counter_profile(w.name, args, rank, attn_tflops / PEAK_BF16_TFLOPS),
         },
         "merge": {
             "kernel": "lse_merge_kernel", "bound": "hbm", "ms": round(merge_ms, 4),
