@@ -158,6 +158,36 @@ def test_sequence_order_output(L, P, C, Hq, Hkv, seed):
     compare(f64(O2[:R]), f64(LSE2[:R]), Or, Lr, "one launch")
 
 
+@pytest.mark.parametrize("L,P,C,seed", [(1100, 0, 2, 91), (1300, 256, 2, 92), (900, 0, 1, 93)])
+def test_exact_redo_on_every_tile(L, P, C, seed):
+    """Logits that rise by more than 2^12 (in base-2 units) from one 32-key
+    tile to the next for the query heads of KV head 0: every tile's
+    probabilities pass the running max's bound, so each tile is redone
+    exactly (O and both row sums rescaled).  KV head 1's logits fall instead
+    (the first tile's max holds for the whole walk)."""
+    Hq, Hkv = 8, 2
+    prob = Problem(L, P, C, Hq, Hkv, seed)
+    pos = torch.arange(prob.R, dtype=torch.float32) * 0.125
+    k = prob.k.float()
+    k[:, 0, 0] = pos
+    k[:, 1, 0] = -pos
+    q = prob.q.float()
+    q[:, :, 0] = 40.0          # 40 * 0.125 * 32 / sqrt(128) * log2(e) = 20.4 per tile
+    prob.k = k.to(torch.bfloat16)
+    prob.q = q.to(torch.bfloat16)
+    # The premise, on the host: for the last query of KV head 0's first
+    # query head, each 32-key tile's largest logit exceeds the previous
+    # tile's by more than 13 in base-2 units (2^13 > 2^16 / 16 lane keys).
+    d = prob.np()
+    x = d["k"][:, 0, :] @ d["q"][-1, 0, :] / math.sqrt(128) / math.log(2)
+    tmax = np.array([x[i:i + 32].max() for i in range(0, prob.R - 31, 32)])
+    assert np.all(np.diff(tmax) > 13.0)
+    for r in range(C):
+        o, lse, _, _ = prob.gpu_rank(r)
+        Or, Lr = prob.oracle_rank(r)
+        compare(f64(o), f64(lse), Or, Lr, f"rank {r}")
+
+
 # Launches with few work items, so the key walks are split into pieces of
 # >= 32 tiles whose partials are merged in the workspace: a long cached
 # prefix under a short suffix (the prefix-hit case), and a small-head shard
