@@ -23,11 +23,16 @@
 //     row max and row sum are in-lane plus one exchange with lane ^ 32, and
 //     the probabilities feed O^T += V^T P^T directly from registers.  V^T
 //     fragments come from the key-major V tile through ds_read_b64_tr_b16.
+//     The sum of the bf16-rounded probabilities, which normalises O, is one
+//     more small MFMA per 16-key step over the same P fragments.
+//   * Each row goes where the descriptor says: the rank's local row, or its
+//     suffix index (the restore to sequence order in the kernel's stores).
 //   * Software pipeline: iteration j runs O += V_{j-1}^T P_{j-1}, the
 //     softmax of S_j and S_{j+1} = K_{j+1} Q^T -- three independent streams
 //     -- as one fixed sequence of MFMA slots with the softmax dealt out
-//     between them.  Iterations go in pairs that share one workgroup barrier and swap
-//     the two score register sets; each iteration loads tile j+5 into LDS.
+//     between them.  Iterations go in pairs that share one workgroup barrier
+//     and swap the two score register sets; each iteration loads tile j+5
+//     into LDS.
 //   * LDS tiles are stored by 16-key halves and 16-byte columns: column c of
 //     a half holds head-dim chunk c (8 values) of its 16 keys, key k at slot
 //     k ^ 4(c % 4).  The K reads (16 keys, one column) and the transposed V
