@@ -32,7 +32,9 @@
  *     partial's keys, LSE = ln sum_j e^{x_j} (natural log, x_j = scale*q.k).
  *     A row that sees no key has O = 0 and LSE = -inf.
  *   - The caller owns every buffer and the stream.  No call allocates device
- *     memory, synchronises the device, or keeps pointers after returning.
+ *     memory, synchronises the device, or keeps pointers after returning
+ *     (cp_attn_partial_noalloc waits for its stream before reusing its
+ *     scratch, as it states).
  *     Launching calls are asynchronous on `stream` (a hipStream_t; NULL is the
  *     null stream) and return after host-side validation and the launch.
  *   - Errors: every call returns CP_OK (0) or a negative status, checks its
