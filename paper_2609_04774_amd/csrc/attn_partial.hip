@@ -7,9 +7,10 @@
 //
 // How (FlashAttention-2 style online softmax, Dao 2023, with the running
 // max/sum recurrence of Milakov & Gimelshein 2018):
-//   * A workgroup of 8 wave64s (two per SIMD) owns 256 (query, head) rows
+//   * A workgroup of 8 wave64s (two per SIMD) owns 384 (query, head) rows
 //     that share one KV head: `heads_per_wg` query heads x `q_per_wg`
-//     consecutive positions.  Each wave owns one block of 32 rows.  Two waves
+//     consecutive positions.  Each wave owns three blocks of 16 rows, so
+//     every K and V fragment read from LDS feeds three MFMAs.  Two waves
 //     per SIMD let one wave's vector and scalar work issue while the other's
 //     matrix work runs (a single wave issues one instruction at a time,
 //     whatever its type); the 256 registers per lane this leaves a wave hold
@@ -19,12 +20,12 @@
 //     never visited; only tiles that cross the diagonal or a range end are
 //     masked.  A work item that sees no key writes its empty result and exits.
 //   * Scores are computed transposed, S^T = K Q^T, with
-//     v_mfma_f32_32x32x16_bf16: a lane then holds one query's column, so the
-//     row max and row sum are in-lane plus one exchange with lane ^ 32, and
+//     v_mfma_f32_16x16x32_bf16: a lane then holds 8 keys of one query per
+//     16-row block (the other 24 are in lanes l ^ 16, l ^ 32, l ^ 48), and
 //     the probabilities feed O^T += V^T P^T directly from registers.  V^T
 //     fragments come from the key-major V tile through ds_read_b64_tr_b16.
 //     The sum of the bf16-rounded probabilities, which normalises O, is one
-//     more small MFMA per 16-key step over the same P fragments.
+//     more MFMA per block over the same P fragments.
 //   * Each row goes where the descriptor says: the rank's local row, or its
 //     suffix index (the restore to sequence order in the kernel's stores).
 //   * Software pipeline: iteration j runs O += V_{j-1}^T P_{j-1}, the
@@ -35,10 +36,11 @@
 //     into LDS.
 //   * LDS tiles are stored by 16-key halves and 16-byte columns: column c of
 //     a half holds head-dim chunk c (8 values) of its 16 keys, key k at slot
-//     k ^ 4(c % 4).  The K reads (16 keys, one column) and the transposed V
-//     reads (4 keys, four columns) then hit every bank once, and each lane's
-//     fragment addresses differ only by constants, so the 24 LDS reads of one
-//     tile's 16 fragments need four address registers.
+//     k ^ 8(c % 2).  The K reads (16 keys, one column per 16 lanes) and the
+//     transposed V reads (8 keys, two columns per 32 lanes) then hit every
+//     bank once, and each lane's fragment addresses differ only by
+//     constants, so the 24 LDS reads of one tile's 16 fragments need two
+//     address registers.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -58,7 +60,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;                    // wave64s per workgroup, two per SIMD
-constexpr int kNB = 1;                       // blocks of 32 rows per wave
+constexpr int kNB = 3;                       // blocks of 16 rows per wave
+constexpr int kBlockRows = 16;
 constexpr int kTileKeys = 32;
 constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
 constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
@@ -67,14 +70,13 @@ constexpr int kTileBytes = kTileKeys * kRowBytes;
 
 // LDS byte offset of head-dim chunk c (16 bytes) of tile key `key` within a
 // tile buffer (64 banks x 4 bytes on gfx950).  A half (16 keys) is 16
-// columns of 256 bytes; in column c, key k sits at slot k ^ 4(c % 4).  Any 16
-// keys of one column fill 256 bytes (every bank once), and keys k0..k0+3
-// (k0 % 4 == 0) of four columns c0..c0+3 (c0 % 4 == 0) occupy 16 distinct
-// slots.
+// columns of 256 bytes; in column c, key k sits at slot k ^ 8(c % 2).  Any 16
+// keys of one column fill 256 bytes (every bank once), and keys k0..k0+7
+// (k0 % 8 == 0) of two columns 2c, 2c + 1 occupy 16 distinct slots.
 constexpr int kHalfBytes = 16 * kRowBytes;
 constexpr int kColBytes = 16 * 16;
 __device__ __forceinline__ int lds_off(int key, int c) {
-  return (key >> 4) * kHalfBytes + c * kColBytes + (((key & 15) ^ (4 * (c & 3))) << 4);
+  return (key >> 4) * kHalfBytes + c * kColBytes + (((key & 15) ^ (8 * (c & 1))) << 4);
 }
 
 __device__ __forceinline__ s16x4 ds_read_tr16(const unsigned char* p) {
@@ -166,7 +168,7 @@ __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
 // This wave's share of one K/V tile load, prepared ahead of the slots that
 // issue it: 1 KB of K and 1 KB of V, i.e. four LDS columns (4g .. 4g+3, g =
 // wave % 4) of tile half wave / 4.  Lane l fills slot l % 16 of column
-// 4g + l/16, so it carries that column's chunk of half key (l % 16) ^ 4(l/16)
+// 4g + l/16, so it carries that column's chunk of half key (l % 16) ^ 8((l/16) % 2)
 // (see lds_off).  The address is a wave-uniform base (tile start, KV head)
 // plus a per-lane offset `lane_off` = row_in_tile * row_stride + 16 * column.
 // In the last tile of a suffix range, rows past the visible end read the
@@ -239,30 +241,47 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
 }
 
-__device__ __forceinline__ float xmax32(float x) {
-  // Max with the lane 32 apart (the other half of the same query's keys).
+// Max / sum over the four lanes that hold one query (l, l ^ 16, l ^ 32, l ^
+// 48: the four row groups of a 16x16 result), by two lane-swap exchanges.
+__device__ __forceinline__ float swap16_max(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                            false, false);
+  return __builtin_elementwise_maximum(__builtin_bit_cast(float, (unsigned)r[0]),
+                                      __builtin_bit_cast(float, (unsigned)r[1]));
+}
+
+__device__ __forceinline__ float swap32_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
                                             false, false);
   return __builtin_elementwise_maximum(__builtin_bit_cast(float, (unsigned)r[0]),
                                       __builtin_bit_cast(float, (unsigned)r[1]));
 }
 
-__device__ __forceinline__ float xsum32(float x) {
+__device__ __forceinline__ float swap16_sum(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                            false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+__device__ __forceinline__ float swap32_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
                                             false, false);
   return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
 }
 
+__device__ __forceinline__ float quad_max(float x) { return swap32_max(swap16_max(x)); }
+__device__ __forceinline__ float quad_sum(float x) { return swap32_sum(swap16_sum(x)); }
+
 // Probabilities of a tile are taken against the running max m of the tiles
 // before it, without looking at the tile's own scores first: p = 2^(x - m).
 // They stay exact relative to each other whatever their size (fp32 and bf16
 // keep 24 and 8 significant bits at any exponent), so m only has to move
-// when p could overflow.  A tile whose fp32 sum of a lane's 16 probabilities
-// exceeds 2^16 (a score more than ~2^12 above m, or the first visible key
-// of a query) is redone exactly: its scores recomputed from the K tile
-// still in LDS, their max taken, O and the sums rescaled, the probabilities
-// taken against the new max.  With probabilities below 2^16 nothing
-// overflows for any |v| below 2^100.
+// when p could overflow.  A tile whose fp32 sum of a lane's 8 probabilities
+// of one query exceeds 2^16 (a score more than ~2^13 above m, or the first
+// visible key of a query) is redone exactly: its scores recomputed from the
+// K tile still in LDS, their max taken, O and the sums rescaled, the
+// probabilities taken against the new max.  With probabilities below 2^16
+// nothing overflows for any |v| below 2^100.
 constexpr float kMaxTileSum = 65536.f;
 // The running max is kept in units of the exponent (score * scale * log2 e)
 // and starts at a finite "nothing seen" value far below any real score's:
@@ -276,93 +295,97 @@ constexpr float kLn2 = 0.69314718055994531f;
 
 // Per-lane LDS byte offsets of the fragments in buffer 0 (buffer b adds
 // b * kTileBytes: one scalar-plus-vector add per offset and tile; the rest
-// are instruction immediates).
-//   K (A operand of S^T = K Q^T): for step ds the lane reads tile key l32,
-//   chunk c = 2ds + half.  c % 4 = 2(ds % 2) + half, so
-//   K(ds) = k[ds % 2] + (ds / 2) * 1024.
-//   V (A operand of O^T += V^T P^T, transposed 64-bit reads): for k-step ks
-//   and head-dim block db the group's 16 lanes read keys
-//   16ks + 8r + 4half + i/4 (r = 0, 1: the two 8-byte halves of the
-//   fragment) at head-dim 32db + 16(group&1) + 4(i%4), i.e. chunk
-//   c = 4db + cc, cc = 2(group&1) + (i%4)/2, byte 8(i%2) of it.  c % 4 = cc
-//   for every db, so V(db, ks, r) = v[r] + db * 1024 + ks * 4096 (v includes
-//   the start of the V buffers, kBufs * kTileBytes).
+// are instruction immediates).  Lane l = 16g + i.
+//   K (A operand of S^T = K Q^T, 16 keys x 32 head-dims): for key half kb
+//   and head-dim step ds the lane reads key i of half kb, chunk c = 4ds + g:
+//   K(kb, ds) = k + kb * 4096 + ds * 1024 (c % 2 = g % 2 for every ds).
+//   V (A operand of O^T += V^T P^T, 16 head-dims x 32 keys, transposed
+//   64-bit reads): for head-dim block db the group's 16 lanes read keys
+//   16r + 4g + i/4 (r = 0, 1: the fragment's two 8-byte halves, one per key
+//   half) at head-dims 16db + 4(i % 4), i.e. chunk c = 2db + (i % 4)/2, byte
+//   8(i % 2) of it; lane i receives head-dim 16db + i of those 4 keys.
+//   c % 2 = (i % 4)/2 for every db, so V(db, r) = v + r * 4096 + db * 512
+//   (v includes the start of the V buffers, kBufs * kTileBytes).
+// The P^T operand of a lane (query i, k = 8g .. 8g+7) then holds keys
+// 4g .. 4g+3 of half 0 and of half 1 -- exactly the scores the lane holds
+// (rows 4g .. 4g+3 of the two S^T results), so P never leaves the lane.
 struct FragOffsets {
-  uint32_t k[2];
-  uint32_t v[2];
+  uint32_t k;
+  uint32_t v;
 };
 
 __device__ __forceinline__ FragOffsets frag_offsets(int lane) {
   FragOffsets f;
-  const int l32 = lane & 31, half = lane >> 5, grp = lane >> 4, gi = lane & 15;
-#pragma unroll
-  for (int e = 0; e < 2; ++e) f.k[e] = (uint32_t)lds_off(l32, 2 * e + half);
-  const int cc = 2 * (grp & 1) + ((gi & 3) >> 1);
-#pragma unroll
-  for (int r = 0; r < 2; ++r)
-    f.v[r] = (uint32_t)(kBufs * kTileBytes + lds_off(8 * r + 4 * half + (gi >> 2), cc) + 8 * (gi & 1));
+  const int g = lane >> 4, i = lane & 15;
+  f.k = (uint32_t)lds_off(i, g);
+  f.v = (uint32_t)(kBufs * kTileBytes + lds_off(4 * g + (i >> 2), (i & 3) >> 1) + 8 * (i & 1));
   return f;
 }
 
-__device__ __forceinline__ const unsigned char* k_frag_addr(const unsigned char* sk, const FragOffsets& fo, int ds) {
-  return sk + fo.k[ds & 1] + (ds >> 1) * 4 * kColBytes;
+__device__ __forceinline__ const unsigned char* k_frag_addr(const unsigned char* sk, const FragOffsets& fo, int q) {
+  // q = 2 ds + kb (the order the region walks the eight K fragments)
+  return sk + fo.k + (q & 1) * kHalfBytes + (q >> 1) * 4 * kColBytes;
 }
 
-__device__ __forceinline__ bf16x8 v_frag(const unsigned char* sv, const FragOffsets& fo, int ks, int db) {
-  const int c = db * 4 * kColBytes + ks * kHalfBytes;
-  const s16x4 lo4 = ds_read_tr16(sv + fo.v[0] + c);
-  const s16x4 hi4 = ds_read_tr16(sv + fo.v[1] + c);
+__device__ __forceinline__ bf16x8 v_frag(const unsigned char* sv, const FragOffsets& fo, int db) {
+  const int c = db * 2 * kColBytes;
+  const s16x4 lo4 = ds_read_tr16(sv + fo.v + c);
+  const s16x4 hi4 = ds_read_tr16(sv + fo.v + kHalfBytes + c);
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// One step of S^T = K Q^T.  Every operand lives in VGPRs, and the compiler
-// sees the instruction, so it keeps the matrix-core hazards (result reads,
-// operand overwrites) itself.
-__device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& k, const bf16x8& q, bool first) {
-  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k, q, first ? f32x16{} : acc, 0, 0, 0);
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// S^T = K Q^T for one 32-key tile (the prologue's first tile).
-__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[kNB][8],
-                                        f32x16 (&s)[kNB]) {
+// Scores of one tile: s[kb][b] = S^T of key half kb and query block b;
+// register r of it is key 16kb + 4g + r of the tile.
+typedef f32x4 Scores[2][kNB];
+
+// One step of S^T = K Q^T (K fragment q = 2ds + kb) for the three blocks.
+// Every operand lives in VGPRs, and the compiler sees the instructions, so
+// it keeps the matrix-core hazards (result reads, operand overwrites) itself.
+__device__ __forceinline__ void qk_step(Scores& s, const bf16x8& k, const bf16x8 (&qf)[kNB][4], int q) {
+  const int kb = q & 1, ds = q >> 1;
 #pragma unroll
-  for (int ds = 0; ds < 8; ++ds) {
-    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, ds));
+  for (int b = 0; b < kNB; ++b) s[kb][b] = mfma16(k, qf[b][ds], ds == 0 ? f32x4{} : s[kb][b]);
+}
+
+// S^T = K Q^T for one 32-key tile (the prologue's first tile, and redos).
+__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[kNB][4],
+                                        Scores& s) {
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) mfma_qk(s[b], kf, qf[b][ds], ds == 0);
+  for (int q = 0; q < 8; ++q) qk_step(s, *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, q)), qf, q);
+}
+
+// O^T += V^T P^T for one 32-key tile (the last one), with the bf16 row sums.
+__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB],
+                                        f32x4 (&o)[8][kNB], const bf16x8& ones, f32x4 (&psum)[kNB]) {
+#pragma unroll
+  for (int db = 0; db < 8; ++db) {
+    const bf16x8 vf = v_frag(sv, fo, db);
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) o[db][b] = mfma16(vf, pf[b], o[db][b]);
   }
+#pragma unroll
+  for (int b = 0; b < kNB; ++b) psum[b] = mfma16(ones, pf[b], psum[b]);
 }
 
-// O^T += V^T P^T for one 32-key tile (the last one).
-__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB][2],
-                                        f32x16 (&o)[4][kNB], const bf16x8& sel, f32x4& psum) {
-#pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-    for (int db = 0; db < 4; ++db) {
-      const bf16x8 vf = v_frag(sv, fo, ks, db);
-#pragma unroll
-      for (int b = 0; b < kNB; ++b) o[db][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][ks], o[db][b], 0, 0, 0);
-    }
-    psum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[0][ks], psum, 0, 0, 0);
-  }
-}
-
-// Masks keys at tile offsets >= lim[b]; score register r is tile key
-// (r/4)*8 + 4*half + r%4.
-__device__ __forceinline__ void mask_tile(f32x16 (&s)[kNB], int half, const int (&lim)[kNB]) {
-  // Compare the constant part of the offset with lim - 4*half, so that no
+// Masks keys at tile offsets >= lim[b]; register r of s[kb][b] is tile key
+// 16kb + 4g + r.
+__device__ __forceinline__ void mask_tile(Scores& s, int g, const int (&lim)[kNB]) {
+  // Compare the constant part of the offset with lim - 4g, so that no
   // per-register offsets need to be kept in registers.
-  int limh[kNB];
+  int limg[kNB];
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) limh[b] = lim[b] - half * 4;
+  for (int b = 0; b < kNB; ++b) limg[b] = lim[b] - 4 * g;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int off = (r >> 2) * 8 + (r & 3);
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int b = 0; b < kNB; ++b)
-      if (off >= limh[b]) s[b][r] = -INFINITY;
-  }
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int b = 0; b < kNB; ++b)
+        if (16 * kb + r >= limg[b]) s[kb][b][r] = -INFINITY;
 }
 
 // Keys at tile offsets >= lim are past the range end (hi) or after the
@@ -381,25 +404,26 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
   }
 }
 
-// One iteration's matrix and vector work as a fixed sequence of 16 MFMA
-// slots: slots 0-7 add P_{j-1} V_{j-1} (V fragment = slot: k-step slot/4,
-// d-block slot%4), slots 8-15 compute S_{j+1} = K_{j+1} Q^T (K step slot -
-// 8).  The softmax of S_j is cut into units of roughly equal VALU time and
-// dealt out over the slots, so that every MFMA has vector work to overlap
-// with.  LDS fragments are read three slots ahead in one continuous stream:
-// the last three slots read the next iteration's first V fragments (of tile
-// j, published since before this pair of iterations), so no iteration starts
-// by waiting for a fresh LDS read.  The two loads of tile j+5 (K rows, then
-// V rows) go out at slots 1 and 9.  Scheduling barriers keep the slots in
-// this order.  The other wave on the same SIMD runs the same sequence
-// shifted in time, so one wave's vector and scalar work issues while the
-// other's matrix work runs.
+// One iteration's matrix and vector work as a fixed sequence of 16 slots,
+// each with one LDS fragment and three MFMAs (one per query block): slots
+// 0-7 add P_{j-1} V_{j-1} (V fragment = head-dim block slot), slots 8-15
+// compute S_{j+1} = K_{j+1} Q^T (K fragment slot - 8); slots 2, 4 and 6 also
+// take block (slot - 2)/2's bf16 row sums.  The softmax of S_j is cut into
+// units of roughly equal VALU time and dealt out over the slots, so that
+// every MFMA has vector work to overlap with.  LDS fragments are read three
+// slots ahead in one continuous stream: the last three slots read the next
+// iteration's first V fragments (of tile j, published since before this
+// pair of iterations), so no iteration starts by waiting for a fresh LDS
+// read.  The two loads of tile j+5 (K rows, then V rows) go out at slots 1
+// and 9.  Scheduling barriers keep the slots in this order.  The other wave
+// on the same SIMD runs the same sequence shifted in time, so one wave's
+// vector and scalar work issues while the other's matrix work runs.
 //
-// Units: eight times (two exponentials, one pack-and-sum) for score pairs,
+// Units: twelve times (two exponentials, one pack-and-sum) for score pairs,
 // against the running max (see kMaxTileSum).  The overflow check, and the
 // exact redo of a tile in the rare case that it fails, follow the region.
 constexpr int kSlots = 16;
-constexpr int kSlotFirstUnit[kSlots + 1] = {0, 2, 3, 5, 6, 8, 9, 11, 12, 14, 15, 17, 18, 20, 21, 23, 24};
+constexpr int kUnits = 36;
 constexpr int kLookahead = 3;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -411,53 +435,56 @@ __device__ __forceinline__ void pin(const T& x) {
 }
 
 struct SoftmaxState {
-  float rs;       // fp32 sum of this tile's probabilities
-  bf16x2 pp[8];
+  float rs[kNB];      // fp32 sum of this tile's probabilities, per block
+  bf16x2 pp[kNB][4];  // bf16 pairs: [half 0 regs 0-1, 2-3, half 1 regs 0-1, 2-3]
 };
 
-// Pair t of the tile's 16 scores (registers 2t, 2t+1, already
-// exponentiated): rounded to bf16 once (the P operand of O += V P), and
-// added to the tile's fp32 sum (the LSE's).  The sum of the bf16-rounded
-// values, which normalises O, is taken by an MFMA over the P fragments
-// (psum in the kernel): a dot-product instruction here would share the
-// matrix pipes with the tile's MFMAs and cost far more issue time.
-__device__ __forceinline__ void pack_and_sum(int t, const f32x16& s, SoftmaxState& st) {
-  const bf16x2 pp = bf16x2{(__bf16)s[2 * t], (__bf16)s[2 * t + 1]};
-  st.pp[t] = pp;
+// Pair t of block b's 8 scores (t = 2 kb + r/2, registers r, r+1 of half
+// kb, already exponentiated): rounded to bf16 once (the P operand of O += V
+// P), and added to the block's fp32 sum (the LSE's).  The sum of the
+// bf16-rounded values, which normalises O, is taken by an MFMA over the P
+// fragments (psum in the kernel): a dot-product instruction here would share
+// the matrix pipes with the tile's MFMAs and cost far more issue time.
+__device__ __forceinline__ void pack_and_sum(int b, int t, const Scores& s, SoftmaxState& st) {
+  const int kb = t >> 1, r = 2 * (t & 1);
+  const bf16x2 pp = bf16x2{(__bf16)s[kb][b][r], (__bf16)s[kb][b][r + 1]};
+  st.pp[b][t] = pp;
   if (t == 0)
-    st.rs = s[0] + s[1];
+    st.rs[b] = s[kb][b][r] + s[kb][b][r + 1];
   else
-    st.rs += s[2 * t] + s[2 * t + 1];
-  pin(st.rs);
+    st.rs[b] += s[kb][b][r] + s[kb][b][r + 1];
+  pin(st.rs[b]);
   pin(pp);
 }
 
-__device__ __forceinline__ void softmax_unit(int u, f32x16& s, SoftmaxState& st, float m_run, float sl2) {
-  const int t = u / 3, kind = u % 3;
+// Unit u: pair t = (u / 3) % 4 of block b = u / 12; kind u % 3 (0, 1: one
+// exponential each; 2: pack and sum).
+__device__ __forceinline__ void softmax_unit(int u, Scores& s, SoftmaxState& st, const float (&m_run)[kNB],
+                                             float sl2) {
+  const int b = u / 12, t = (u / 3) % 4, kind = u % 3;
   if (kind < 2) {
-    const int i = 2 * t + kind;
-    const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i], sl2, -m_run));
+    const int kb = t >> 1, r = 2 * (t & 1) + kind;
+    const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][b][r], sl2, -m_run[b]));
     pin(x);
-    s[i] = x;
+    s[kb][b][r] = x;
   } else {
-    pack_and_sum(t, s, st);
+    pack_and_sum(b, t, s, st);
   }
 }
 
-// Max of a lane's 16 scores and of the other lane half's (the same query's
-// other 16 keys), in exponent units.
-__device__ __forceinline__ float tile_max(const f32x16& s, float sl2) {
-  float mx = max3(__builtin_elementwise_maximum(s[0], s[1]), s[2], s[3]);
-#pragma unroll
-  for (int q = 4; q < 16; q += 4) mx = max3(max3(mx, s[q], s[q + 1]), s[q + 2], s[q + 3]);
-  return xmax32(mx) * sl2;
+// Max of block b's scores of one query (a lane's 8 and the three other
+// lanes' 24), in exponent units.
+__device__ __forceinline__ float tile_max(const Scores& s, int b, float sl2) {
+  float mx = max3(__builtin_elementwise_maximum(s[0][b][0], s[0][b][1]), s[0][b][2], s[0][b][3]);
+  mx = max3(max3(mx, s[1][b][0], s[1][b][1]), s[1][b][2], s[1][b][3]);
+  return quad_max(mx) * sl2;
 }
 
-// Fragment g of the region: g < 8 is V^T fragment (k-step g/4, d-block
-// g%4), g >= 8 is K step g - 8.
+// Fragment g of the region: g < 8 is V^T fragment (head-dim block g), g >=
+// 8 is K fragment g - 8.
 __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, const unsigned char* sk,
                                             const FragOffsets& fo) {
-  if (g < 8) return v_frag(sv, fo, g >> 2, g & 3);
+  if (g < 8) return v_frag(sv, fo, g);
   return *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, g - 8));
 }
 
@@ -466,10 +493,11 @@ __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, cons
 // into O.
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
                                                  const unsigned char* sv_next, const FragOffsets& fo,
-                                                 const bf16x8 (&qf)[kNB][8], const bf16x8 (&pf)[kNB][2],
-                                                 f32x16 (&o)[4][kNB], f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB],
-                                                 float m_run, float sl2, const TileLoad& ld, SoftmaxState& st,
-                                                 bf16x8 (&pre)[kLookahead], const bf16x8& sel, f32x4& psum) {
+                                                 const bf16x8 (&qf)[kNB][4], const bf16x8 (&pf)[kNB],
+                                                 f32x4 (&o)[8][kNB], Scores& s_in, Scores& s_out,
+                                                 const float (&m_run)[kNB], float sl2, const TileLoad& ld,
+                                                 SoftmaxState& st, bf16x8 (&pre)[kLookahead], const bf16x8& ones,
+                                                 f32x4 (&psum)[kNB]) {
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = pre[g];
@@ -482,38 +510,51 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
       pre[g - 16] = load_frag(g - 16, sv_next, sk, fo);  // the next iteration's first V fragments
     if ((slot & 7) == 1) issue_load(ld, slot >> 3);
     if (slot < 8) {
-      o[slot & 3][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[slot], pf[0][slot >> 2], o[slot & 3][0], 0, 0, 0);
-      // After a k-step's last P V product: the bf16 row sums of its 16 keys.
-      if ((slot & 3) == 3) psum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[0][slot >> 2], psum, 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < kNB; ++b) o[slot][b] = mfma16(fr[slot], pf[b], o[slot][b]);
+      if (slot >= 2 && (slot & 1) == 0 && (slot - 2) / 2 < kNB) {
+        const int b = (slot - 2) / 2;
+        psum[b] = mfma16(ones, pf[b], psum[b]);
+      }
     } else {
-      mfma_qk(s_out[0], fr[slot], qf[0][slot - 8], slot == 8);
+      qk_step(s_out, fr[slot], qf, slot - 8);
     }
 #pragma unroll
-    for (int u = kSlotFirstUnit[slot]; u < kSlotFirstUnit[slot + 1]; ++u) softmax_unit(u, s_in[0], st, m_run, sl2);
+    for (int u = (slot * kUnits) / kSlots; u < ((slot + 1) * kUnits) / kSlots; ++u)
+      softmax_unit(u, s_in, st, m_run, sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 // The exact redo of tile j (rare; see kMaxTileSum): s holds S_j, recomputed
-// and masked by the caller.  The running max moves to the max of the tile
-// where that is higher, O and the running sums are rescaled by 2^(m_old -
-// m_new) (exactly 1 where it did not move, 0 before a query's first visible
-// key), and the tile's probabilities are taken against the new max.
-__device__ __forceinline__ void exact_softmax(f32x16& s, float& m_run, float& l_run, f32x4& psum,
-                                              f32x16 (&o)[4][kNB], float sl2, SoftmaxState& st) {
-  const float m_new = __builtin_elementwise_maximum(tile_max(s, sl2), m_run);
-  const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-  l_run *= alpha;
-  psum *= alpha;
+// and masked by the caller.  Each block's running max moves to the max of
+// the tile where that is higher, O and the running sums are rescaled by
+// 2^(m_old - m_new) (exactly 1 where it did not move, 0 before a query's
+// first visible key), and the tile's probabilities are taken against the
+// new max.
+__device__ __forceinline__ void exact_softmax(Scores& s, float (&m_run)[kNB], float (&l_run)[kNB],
+                                              f32x4 (&psum)[kNB], f32x4 (&o)[8][kNB], float sl2, SoftmaxState& st) {
 #pragma unroll
-  for (int db = 0; db < 4; ++db) o[db][0] *= alpha;
-  m_run = m_new;
+  for (int b = 0; b < kNB; ++b) {
+    const float m_new = __builtin_elementwise_maximum(tile_max(s, b, sl2), m_run[b]);
+    const float alpha = __builtin_amdgcn_exp2f(m_run[b] - m_new);
+    l_run[b] *= alpha;
+    psum[b] *= alpha;
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k) s[2 * t + k] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * t + k], sl2, -m_new));
-    pack_and_sum(t, s, st);
+    for (int db = 0; db < 8; ++db) o[db][b] *= alpha;
+    m_run[b] = m_new;
   }
+#pragma unroll
+  for (int b = 0; b < kNB; ++b)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int kb = t >> 1, r = 2 * (t & 1) + k;
+        s[kb][b][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][b][r], sl2, -m_run[b]));
+      }
+      pack_and_sum(b, t, s, st);
+    }
 }
 
 // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
@@ -534,8 +575,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int half = lane >> 5;
-  const int l32 = lane & 31;
+  const int g4 = lane >> 4;   // row group of the 16x16 results
+  const int l16 = lane & 15;  // query of the lane within a block
 
   // Positions are below 2^30 (checked on the host): 32 bits suffice.
   const int q_begin = (int)(it.chunk ? d.q_begin[1] : d.q_begin[0]);
@@ -546,7 +587,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const int Hkv = p.Hkv;
   const int kvh = it.head_group / p.groups_per_kv;
   const int head0 = kvh * (Hq / Hkv) + (it.head_group % p.groups_per_kv) * p.heads_per_wg;
-  const int qblocks_per_head = p.q_per_wg >> 5;
+  const int qblocks_per_head = p.q_per_wg / kBlockRows;
   const int qb0 = it.q_block * p.q_per_wg;
   const int wg_last = (qb0 + p.q_per_wg < q_len ? qb0 + p.q_per_wg : q_len) - 1;
   const int wg_pos_hi = q_begin + wg_last;
@@ -559,10 +600,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   for (int b = 0; b < kNB; ++b) {
     const int bi = kNB * wave + b;
     head_b[b] = head0 + bi / qblocks_per_head;
-    const int qo = (bi % qblocks_per_head) * 32;
-    qrel_b[b] = qo + l32;
+    const int qo = (bi % qblocks_per_head) * kBlockRows;
+    qrel_b[b] = qo + l16;
     valid_b[b] = qb0 + qrel_b[b] < q_len;
-    const int blo = qb0 + qo, bhi = (qb0 + qo + 31 < wg_last ? qb0 + qo + 31 : wg_last);
+    const int blo = qb0 + qo, bhi = (qb0 + qo + kBlockRows - 1 < wg_last ? qb0 + qo + kBlockRows - 1 : wg_last);
     if (blo <= wg_last) {
       wave_lo = (q_begin + blo < wave_lo) ? q_begin + blo : wave_lo;
       wave_hi = (q_begin + bhi > wave_hi) ? q_begin + bhi : wave_hi;
@@ -603,9 +644,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       const int64_t row = ooff + qb0 + qrel_b[b];
       float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
 #pragma unroll
-      for (int c = 0; c < kHeadDim / 8; ++c)
-        *reinterpret_cast<float4*>(orow + c * 8 + half * 4) = float4{0.f, 0.f, 0.f, 0.f};
-      if (half == 0) d.lse[row * Hq + head_b[b]] = -INFINITY;
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(orow + db * 16 + g4 * 4) = float4{0.f, 0.f, 0.f, 0.f};
+      if (g4 == 0) d.lse[row * Hq + head_b[b]] = -INFINITY;
     }
     return;
   }
@@ -642,7 +683,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // Per-lane part of the tile load addresses (see prep_tile): column
   // 4(wave % 4) + lane / 16 of half wave / 4, slot lane % 16.
   const int row_stride = Hkv * kHeadDim * 2;
-  const int lane_row = (wave >> 2) * 16 + ((lane & 15) ^ (4 * (lane >> 4)));
+  const int lane_row = (wave >> 2) * 16 + ((lane & 15) ^ (8 * ((lane >> 4) & 1)));
   const uint32_t lane_col = (uint32_t)((4 * (wave & 3) + (lane >> 4)) * 16);
   const uint32_t lane_off = (uint32_t)(lane_row * row_stride) + lane_col;
   const uint32_t lds0 = lds_addr(smem);
@@ -657,18 +698,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   };
   if (n_tiles > 0) issue_tile(load_of(t_first, t_first & (kBufs - 1)));
 
-  // Query fragments (B operand of S^T = K Q^T): lane holds 8 consecutive
-  // head-dim values of its query, for each of the 8 steps of 16 along D.
-  // Rows past the chunk's end are zero and masked out of every tile.
-  bf16x8 qf[kNB][8];
+  // Query fragments (B operand of S^T = K Q^T, 32 head-dims x 16 queries):
+  // lane 16g + i holds 8 consecutive head-dim values (8g .. 8g+7 of step ds)
+  // of query i of each block, for each of the 4 steps of 32 along D.  Rows
+  // past the chunk's end are zero and masked out of every tile.
+  bf16x8 qf[kNB][4];
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
     const int64_t qrow_i = loff + (valid_b[b] ? qb0 + qrel_b[b] : qb0);
     const __attribute__((address_space(1))) bf16x8* qrow =
-        (const __attribute__((address_space(1))) bf16x8*)(d.q + (qrow_i * Hq + head_b[b]) * kHeadDim + half * 8);
+        (const __attribute__((address_space(1))) bf16x8*)(d.q + (qrow_i * Hq + head_b[b]) * kHeadDim + g4 * 8);
 #pragma unroll
-    for (int ds = 0; ds < 8; ++ds) {
-      const bf16x8 v = qrow[2 * ds];
+    for (int ds = 0; ds < 4; ++ds) {
+      const bf16x8 v = qrow[4 * ds];
       qf[b][ds] = valid_b[b] ? v : bf16x8{};
     }
   }
@@ -706,34 +748,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
 
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
-  f32x16 o[4][kNB];
+  f32x4 o[8][kNB];
   float m_run[kNB];                            // running max (exponent units)
   float l_run[kNB];                            // sum of the fp32 probabilities (lane's keys)
-  // Sums of the bf16-rounded probabilities, by a 16x16x32 MFMA over the P
-  // fragments: with the P^T fragment read as its B operand, lane l holds
-  // query 16 * ((l / 16) % 2) + l % 16's keys of k-group l / 16 (k = 8 * (l /
-  // 16) + j), so a selector A with A[m][k] = 1 iff (k / 8) % 2 == m % 2 sums
-  // every key of query n (even m) and of query 16 + n (odd m) into C[m][n].
-  // Lane l holds C[4 * (l / 16) + r][l % 16]: r = 0 for query l % 16, r = 1
-  // for query 16 + l % 16.
-  f32x4 psum = f32x4{};
-  bf16x8 sel;
-  {
-    const __bf16 one = (((lane >> 4) & 1) == ((lane & 15) & 1)) ? (__bf16)1.0f : (__bf16)0.0f;
+  // Sums of the bf16-rounded probabilities, by a 16x16x32 MFMA with an
+  // all-ones A over each block's P fragment: every row of psum[b] holds the
+  // sum over the tile's 32 keys of the lane's query, so every lane has its
+  // query's full sum.
+  f32x4 psum[kNB];
+  bf16x8 ones;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sel[e] = one;
-  }
-  bf16x8 pf[kNB][2];                           // P of the previous tile
+  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+  bf16x8 pf[kNB];                              // P of the previous tile
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
 #pragma unroll
-    for (int db = 0; db < 4; ++db) o[db][b] = f32x16{};
+    for (int db = 0; db < 8; ++db) o[db][b] = f32x4{};
     m_run[b] = kNoMax;
     l_run[b] = 0.f;
-    pf[b][0] = pf[b][1] = bf16x8{};
+    psum[b] = f32x4{};
+    pf[b] = bf16x8{};
   }
   // Scores of the current tile alternate between two register sets.
-  f32x16 sa[kNB], sb[kNB];
+  Scores sa, sb;
   const int q0 = q_begin + qb0;
 
   // The first iteration's P V step reads the V buffer before the first
@@ -748,11 +785,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   auto masked_tile = [&](int j) {
     return (j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c;
   };
-  auto mask_if_needed = [&](int j, f32x16 (&s)[kNB]) {
+  auto mask_if_needed = [&](int j, Scores& s) {
     if (masked_tile(j)) {
       int lim[kNB];
       tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
-      mask_tile(s, half, lim);
+      mask_tile(s, g4, lim);
     }
   };
   bf16x8 pre[kLookahead];
@@ -764,7 +801,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     // that the first iteration's probabilities need no redo).
     qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
     mask_if_needed(t_first, sa);
-    m_run[0] = __builtin_elementwise_maximum(tile_max(sa[0], sl2), kNoMax);
+#pragma unroll
+    for (int b = 0; b < kNB; ++b) m_run[b] = __builtin_elementwise_maximum(tile_max(sa, b, sl2), kNoMax);
   }
 
   // Iteration j (tile buffer B = j % kBufs): mask
@@ -790,27 +828,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     cur = ld;
     return ld;
   };
-  auto iteration = [&](int j, f32x16 (&s_in)[kNB], f32x16 (&s_out)[kNB]) {
+  auto iteration = [&](int j, Scores& s_in, Scores& s_out) {
     const int B = j & (kBufs - 1);
     mask_if_needed(j, s_in);
     const TileLoad ld = next_load(j);
     SoftmaxState st;
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes,
-                     smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run[0], sl2, ld, st, pre, sel, psum);
+                     smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run, sl2, ld, st, pre, ones, psum);
     // Rare: some lane's probabilities were too large (its max grew by more
-    // than ~2^12, or it saw its first key).  Redo the tile exactly; its K
+    // than ~2^13, or it saw its first key).  Redo the tile exactly; its K
     // tile is still in buffer B (tile j + 8 is loaded three iterations on).
-    if (__builtin_amdgcn_ballot_w64(!(st.rs <= kMaxTileSum)) != 0) {
+    const bool ok = st.rs[0] <= kMaxTileSum && st.rs[1] <= kMaxTileSum && st.rs[2] <= kMaxTileSum;
+    if (__builtin_amdgcn_ballot_w64(!ok) != 0) {
       qk_tile(smem + B * kTileBytes, fo, qf, s_in);
       mask_if_needed(j, s_in);
-      exact_softmax(s_in[0], m_run[0], l_run[0], psum, o, sl2, st);
+      exact_softmax(s_in, m_run, l_run, psum, o, sl2, st);
     }
-    l_run[0] += st.rs;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-      pf[0][ks] = __builtin_shufflevector(__builtin_shufflevector(st.pp[4 * ks], st.pp[4 * ks + 1], 0, 1, 2, 3),
-                                          __builtin_shufflevector(st.pp[4 * ks + 2], st.pp[4 * ks + 3], 0, 1, 2, 3),
-                                          0, 1, 2, 3, 4, 5, 6, 7);
+    for (int b = 0; b < kNB; ++b) {
+      l_run[b] += st.rs[b];
+      pf[b] = __builtin_shufflevector(__builtin_shufflevector(st.pp[b][0], st.pp[b][1], 0, 1, 2, 3),
+                                      __builtin_shufflevector(st.pp[b][2], st.pp[b][3], 0, 1, 2, 3), 0, 1, 2, 3,
+                                      4, 5, 6, 7);
+    }
   };
 
   // Iterations go in pairs behind one barrier.  At a pair's start every tile
@@ -840,51 +880,42 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   }
   // No tile load may still be writing LDS when the workgroup ends.
   __builtin_amdgcn_s_waitcnt(kWaitVm(0));
-  if (n_tiles > 0 && wave_active) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, sel, psum);
+  if (n_tiles > 0 && wave_active) pv_tile(smem + ((t_stop - 1) & (kBufs - 1)) * kTileBytes, fo, pf, o, ones, psum);
 
-  // Normalise and store: O^T register r of d-block db is head-dim
-  // db*32 + (r/4)*8 + 4*half + r%4 of this lane's query.
+  // Normalise and store: O^T register r of (db, b) is head-dim 16db + 4g + r
+  // of this lane's query of block b.
 #pragma unroll
   for (int b = 0; b < kNB; ++b) {
-    const float lt = xsum32(l_run[b]);
-    const float ltb = ((lane >> 4) & 1) ? psum[1] : psum[0];
+    const float lt = quad_sum(l_run[b]);
+    const float ltb = psum[b][0];
     const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
     const float inv = live ? 1.f / ltb : 0.f;
+    const float lse = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
+    float* orow;
+    float* lrow;
     if (it.piece >= 0) {
       // One piece of a split walk: its partial over its keys goes to the
-      // piece slot (row 32 * block + lane of the work item).
+      // piece slot (row 16 * block + query of the work item).
       unsigned char* slot = p.pieces + (size_t)it.piece * kPieceBytes;
-      const int r = (kNB * wave + b) * 32 + l32;
-      float* orow = reinterpret_cast<float*>(slot) + (size_t)r * kHeadDim;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          float4 v;
-          v.x = o[db][b][4 * q4 + 0] * inv;
-          v.y = o[db][b][4 * q4 + 1] * inv;
-          v.z = o[db][b][4 * q4 + 2] * inv;
-          v.w = o[db][b][4 * q4 + 3] * inv;
-          *reinterpret_cast<float4*>(orow + db * 32 + q4 * 8 + half * 4) = v;
-        }
-      if (half == 0)
-        reinterpret_cast<float*>(slot + kPieceOBytes)[r] = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
-    } else if (valid_b[b]) {
+      const int r = (kNB * wave + b) * kBlockRows + l16;
+      orow = reinterpret_cast<float*>(slot) + (size_t)r * kHeadDim;
+      lrow = reinterpret_cast<float*>(slot + kPieceOBytes) + r;
+    } else {
+      if (!valid_b[b]) continue;
       const int64_t row = ooff + qb0 + qrel_b[b];
-      float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          float4 v;
-          v.x = o[db][b][4 * q4 + 0] * inv;
-          v.y = o[db][b][4 * q4 + 1] * inv;
-          v.z = o[db][b][4 * q4 + 2] * inv;
-          v.w = o[db][b][4 * q4 + 3] * inv;
-          *reinterpret_cast<float4*>(orow + db * 32 + q4 * 8 + half * 4) = v;
-        }
-      if (half == 0) d.lse[row * Hq + head_b[b]] = live ? m_run[b] * kLn2 + logf(lt) : -INFINITY;
+      orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
+      lrow = d.lse + row * Hq + head_b[b];
     }
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      float4 v;
+      v.x = o[db][b][0] * inv;
+      v.y = o[db][b][1] * inv;
+      v.z = o[db][b][2] * inv;
+      v.w = o[db][b][3] * inv;
+      *reinterpret_cast<float4*>(orow + db * 16 + g4 * 4) = v;
+    }
+    if (g4 == 0) *lrow = lse;
   }
 }
 
@@ -903,12 +934,12 @@ __global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restr
   const int r = (blockIdx.x % blocks_per_item) * kMergeRowsPerBlock + (threadIdx.x >> 5);
   const int lane = threadIdx.x & 31;
   const DevDesc& d = descs[sp.desc];
-  // The row's place, as the attention kernel assigns it (block bi, lane l32).
-  const int bi = r >> 5, l32 = r & 31;
-  const int qblocks_per_head = p.q_per_wg >> 5;
+  // The row's place, as the attention kernel assigns it (block bi, query l16).
+  const int bi = r >> 4, l16 = r & 15;
+  const int qblocks_per_head = p.q_per_wg >> 4;
   const int kvh = sp.head_group / p.groups_per_kv;
   const int head = kvh * (p.Hq / p.Hkv) + (sp.head_group % p.groups_per_kv) * p.heads_per_wg + bi / qblocks_per_head;
-  const int qrel = (bi % qblocks_per_head) * 32 + l32;
+  const int qrel = (bi % qblocks_per_head) * 16 + l16;
   const int64_t qb0 = (int64_t)sp.q_block * p.q_per_wg;
   const int64_t q_len = sp.chunk ? d.q_len[1] : d.q_len[0];
   if (qb0 + qrel >= q_len) return;

@@ -24,6 +24,7 @@
 #include <cstring>
 #include <mutex>
 #include <numeric>
+#include <queue>
 #include <string>
 #include <vector>
 
@@ -151,6 +152,79 @@ int to_dev(const cp_partial_desc& x, int idx, DevDesc* out) {
 constexpr int64_t kSplitBelowItems = 512;  // split only launches with fewer non-empty items
 constexpr int64_t kMinPieceTiles = 32;     // 1024 keys: the prologue and merge stay small
 constexpr int64_t kMaxPieces = 64;
+constexpr int kComputeUnits = 256;         // 8 XCDs x 32 compute units
+constexpr int64_t kItemSetupTiles = 4;     // a workgroup's set-up and stores, in tile times
+constexpr double kBalanceSlack = 1.03;
+
+// Balance cuts.  The hardware dispatches workgroups in list order to
+// whichever compute unit frees up first, so a list sorted longest first is an
+// LPT schedule -- but when the long items are not a multiple of the compute
+// units (384-row items of a 4096-row chunk: 344 of them for 256 units), the
+// last round of long items runs on a few units while the rest idle.  This
+// simulates that schedule (item time = its tiles + kItemSetupTiles) and, when
+// its makespan exceeds the ideal (total / units) by more than kBalanceSlack,
+// replays it cutting items: an item that would push the least loaded unit
+// past the ideal gives that unit only the tiles that fill it up, and its
+// remaining tiles go back into the queue as a later item.  Returns each
+// item's interior cut points (tile indices, ascending); none when no cut
+// pays.
+std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles) {
+  std::vector<std::vector<int32_t>> cuts(tiles.size());
+  struct Seg {
+    int64_t len;
+    int32_t item, t0;
+  };
+  auto longer = [](const Seg& a, const Seg& b) { return a.len < b.len || (a.len == b.len && a.item > b.item); };
+  std::priority_queue<Seg, std::vector<Seg>, decltype(longer)> queue(longer);
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
+  int64_t total = 0;
+  std::vector<int64_t> lens;
+  for (size_t i = 0; i < tiles.size(); ++i)
+    if (tiles[i] > 0) {
+      total += tiles[i] + kItemSetupTiles;
+      lens.push_back(tiles[i]);
+    }
+  if (lens.empty()) return cuts;
+  const int64_t ideal = (total + kComputeUnits - 1) / kComputeUnits;
+  const int64_t limit = (int64_t)(ideal * kBalanceSlack);
+  // The schedule without cuts.
+  std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
+  for (int u = 0; u < kComputeUnits; ++u) units.push(0);
+  int64_t makespan = 0;
+  for (int64_t len : lens) {
+    const int64_t t = units.top() + len + kItemSetupTiles;
+    units.pop();
+    units.push(t);
+    makespan = std::max(makespan, t);
+  }
+  if (makespan <= limit) return cuts;
+  // The same schedule with cuts.
+  while (!units.empty()) units.pop();
+  for (int u = 0; u < kComputeUnits; ++u) units.push(0);
+  for (size_t i = 0; i < tiles.size(); ++i)
+    if (tiles[i] > 0) queue.push(Seg{tiles[i], (int32_t)i, 0});
+  while (!queue.empty()) {
+    const Seg s = queue.top();
+    queue.pop();
+    const int64_t load = units.top();
+    units.pop();
+    int64_t take = s.len;
+    if (load + s.len + kItemSetupTiles > limit && (int64_t)cuts[s.item].size() + 1 < kMaxPieces) {
+      // Fill this unit up to the ideal; both parts keep at least
+      // kMinPieceTiles tiles.
+      int64_t room = ideal - load - kItemSetupTiles;
+      room = std::min(room, s.len - kMinPieceTiles);
+      if (room >= kMinPieceTiles) take = room;
+    }
+    units.push(load + take + kItemSetupTiles);
+    if (take < s.len) {
+      cuts[s.item].push_back(s.t0 + (int32_t)take);
+      queue.push(Seg{s.len - take, s.item, s.t0 + (int32_t)take});
+    }
+  }
+  for (auto& c : cuts) std::sort(c.begin(), c.end());
+  return cuts;
+}
 
 // Key tiles of one work item's walk, exactly as the kernel counts them: the
 // paged prefix, then each suffix range clipped to the item's last query.
@@ -222,23 +296,42 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   int64_t piece_tiles = 0;  // 0: no splitting in this launch
   if (target_pieces > 0 && nonempty > 0 && nonempty < kSplitBelowItems && max_tiles >= 4 * kMinPieceTiles)
     piece_tiles = std::max<int64_t>(kMinPieceTiles, (all_tiles + target_pieces - 1) / target_pieces);
+  // Cut points of each item's walk (item = block * n_groups + head group):
+  // equal pieces when few items split for occupancy, else balance cuts.
+  std::vector<std::vector<int32_t>> cuts;
+  if (piece_tiles) {
+    cuts.resize(blocks.size() * n_groups);
+    for (size_t bi = 0; bi < blocks.size(); ++bi) {
+      const int64_t n = std::min<int64_t>(kMaxPieces, blocks[bi].tiles / piece_tiles);
+      for (int g = 0; g < n_groups; ++g)
+        for (int64_t k = 1; k < n; ++k) cuts[bi * n_groups + g].push_back((int32_t)(blocks[bi].tiles * k / n));
+    }
+  } else if (target_pieces > 0) {
+    std::vector<int64_t> tiles(blocks.size() * n_groups);
+    for (size_t bi = 0; bi < blocks.size(); ++bi)
+      for (int g = 0; g < n_groups; ++g) tiles[bi * n_groups + g] = blocks[bi].tiles;
+    cuts = balance_cuts(tiles);
+  }
   out->splits.clear();
   out->n_pieces = 0;
   std::vector<std::vector<Cand>> per_xcd(kXcds);
   int64_t total = 0;
-  for (const Block& b : blocks) {
-    const int64_t n_pieces = piece_tiles ? std::min<int64_t>(kMaxPieces, b.tiles / piece_tiles) : 1;
+  for (size_t bi = 0; bi < blocks.size(); ++bi) {
+    const Block& b = blocks[bi];
     for (int g = 0; g < n_groups; ++g) {
-      if (n_pieces <= 1) {
+      const std::vector<int32_t>* c = cuts.empty() ? nullptr : &cuts[bi * n_groups + g];
+      if (!c || c->empty()) {
         per_xcd[g % kXcds].push_back(Cand{b.keys, WorkItem{b.desc, b.chunk, b.q_block, g, 0, -1, -1, 0}});
         ++total;
         continue;
       }
+      const int64_t n_pieces = (int64_t)c->size() + 1;
       out->splits.push_back(SplitItem{b.desc, b.chunk, b.q_block, g, (int32_t)out->n_pieces, (int32_t)n_pieces});
       for (int64_t k = 0; k < n_pieces; ++k) {
-        const int32_t t0 = (int32_t)(b.tiles * k / n_pieces), t1 = (int32_t)(b.tiles * (k + 1) / n_pieces);
+        const int32_t t0 = k == 0 ? 0 : (*c)[k - 1];
+        const int32_t t1 = k + 1 == n_pieces ? (int32_t)b.tiles : (*c)[k];
         per_xcd[g % kXcds].push_back(
-            Cand{(t1 - t0) * 32, WorkItem{b.desc, b.chunk, b.q_block, g, t0, t1, (int32_t)(out->n_pieces + k), 0}});
+            Cand{(int64_t)(t1 - t0) * 32, WorkItem{b.desc, b.chunk, b.q_block, g, t0, t1, (int32_t)(out->n_pieces + k), 0}});
         ++total;
       }
       out->n_pieces += n_pieces;

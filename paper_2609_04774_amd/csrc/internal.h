@@ -43,7 +43,7 @@ bool plan_equal(const cp_rank_plan& a, const cp_rank_plan& b);
 
 constexpr int kHeadDim = 128;
 constexpr int kBlockTokens = 16;
-constexpr int kRowsPerWG = 256;      // (query, head) rows per workgroup
+constexpr int kRowsPerWG = 384;      // (query, head) rows per workgroup
 
 // One descriptor as the kernel reads it.  Key sets are expressed as global
 // positions: the prefix [0, prefix_keys) through the block table, then up to
@@ -102,8 +102,8 @@ struct SplitItem {
   int32_t n_pieces;
 };
 
-// Workspace of one piece: fp32 O of the work item's 256 rows (row = 32 *
-// block + lane), then their LSE.
+// Workspace of one piece: fp32 O of the work item's 384 rows (row = 16 *
+// block + query), then their LSE.
 constexpr size_t kPieceOBytes = (size_t)kRowsPerWG * kHeadDim * 4;
 constexpr size_t kPieceBytes = kPieceOBytes + (size_t)kRowsPerWG * 4;
 
@@ -114,11 +114,11 @@ struct PartialParams {
   int32_t Hq;
   int32_t Hkv;
   int32_t heads_per_wg;   // query heads of one KV head handled by one workgroup
-  int32_t q_per_wg;       // query positions per workgroup (heads_per_wg * q_per_wg = 256)
+  int32_t q_per_wg;       // query positions per workgroup (heads_per_wg * q_per_wg = 384)
   int32_t groups_per_kv;  // (Hq / Hkv) / heads_per_wg
   float scale_log2;       // softmax scale * log2(e)
   float scale;            // softmax scale
-  int32_t waves_per_wg;   // 8 (one 32-row block per wave)
+  int32_t waves_per_wg;   // 8 (three 16-row blocks per wave)
   unsigned char* pieces;  // piece slots (kPieceBytes each), or null when nothing is split
   const SplitItem* splits;
   int32_t n_splits;

@@ -277,16 +277,23 @@ def test_workspace_size_grows_with_work():
 def test_workspace_holds_piece_slots_for_split_walks():
     """Few query rows over a long cached prefix: the launch has few work items,
     so each item's key walk is split into pieces and the workspace grows by
-    one slot (fp32 O and LSE of 256 rows) per piece.  A launch with many items
-    is never split."""
-    piece = 256 * 128 * 4 + 256 * 4
+    one slot (fp32 O and LSE of 384 rows) per piece.  A launch whose long
+    items do not fill the 256 compute units evenly has some of them cut to
+    balance the schedule; one with many small items is never split."""
+    piece = 384 * 128 * 4 + 384 * 4
     # 64 rows, 4 of 32 query heads per workgroup -> 16 items of 2049-2050
     # tiles; about 1024 pieces in all: pieces of 33 tiles, 62 per item.
     split = cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8)
     assert 16 * 62 * piece <= split < 16 * 62 * piece + (1 << 20)
-    # The 32K Llama-3-8B rank-0 shard: 4096 items, no pieces.
-    whole = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
-    assert whole < piece
+    # The 32K Llama-3-8B rank-0 shard: 688 items of 96 positions x 4 heads,
+    # 344 of them long (chunk 7); 88 of those are cut in three, so that each
+    # compute unit ends near the ideal.
+    balanced = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
+    assert 264 * piece <= balanced < 264 * piece + (1 << 20)
+    # The 70B shard's eight pass-KV partials: 21888 items of 32 bytes and
+    # the descriptors, no pieces.
+    many = cp.workspace_size([_desc(R=131072, C=8, kv_rank=s) for s in range(8)], 64, 8)
+    assert 21888 * 32 <= many < 21888 * 32 + 8192
 
 
 def _merge_status(n_parts=2, n_tokens=4, H=2, D=128, out=FAKE, lse_out=FAKE * 2, restore=None,
