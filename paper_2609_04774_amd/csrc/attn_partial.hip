@@ -410,8 +410,8 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 // compute S_{j+1} = K_{j+1} Q^T (K fragment slot - 8); slots 2, 4 and 6 also
 // take block (slot - 2)/2's bf16 row sums.  The softmax of S_j is cut into
 // units of roughly equal VALU time and dealt out over the slots, so that
-// every MFMA has vector work to overlap with.  LDS fragments are read three
-// slots ahead in one continuous stream: the last three slots read the next
+// every MFMA has vector work to overlap with.  LDS fragments are read two
+// slots ahead in one continuous stream: the last two slots read the next
 // iteration's first V fragments (of tile j, published since before this
 // pair of iterations), so no iteration starts by waiting for a fresh LDS
 // read.  The two loads of tile j+5 (K rows, then V rows) go out at slots 1
@@ -424,7 +424,7 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 // exact redo of a tile in the rare case that it fails, follow the region.
 constexpr int kSlots = 16;
 constexpr int kUnits = 36;
-constexpr int kLookahead = 3;
+constexpr int kLookahead = 2;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
 // reads it stays in program order with the scheduling barriers, so the
