@@ -153,7 +153,8 @@ constexpr int64_t kSplitBelowItems = 512;  // split only launches with fewer non
 constexpr int64_t kMinPieceTiles = 32;     // 1024 keys: the prologue and merge stay small
 constexpr int64_t kMaxPieces = 64;
 constexpr int kComputeUnits = 256;         // 8 XCDs x 32 compute units
-constexpr int64_t kItemSetupTiles = 4;     // a workgroup's set-up and stores, in tile times
+constexpr int64_t kItemSetupTiles = 16;    // a workgroup's set-up and stores, in tile times
+constexpr int64_t kMinBalancePiece = 256;  // tiles of the smaller part of a balance cut
 constexpr double kBalanceSlack = 1.03;
 
 // Balance cuts.  The hardware dispatches workgroups in list order to
@@ -165,10 +166,11 @@ constexpr double kBalanceSlack = 1.03;
 // its makespan exceeds the ideal (total / units) by more than kBalanceSlack,
 // replays it cutting items: an item that would push the least loaded unit
 // past the ideal gives that unit only the tiles that fill it up, and its
-// remaining tiles go back into the queue as a later item.  Returns each
-// item's interior cut points (tile indices, ascending); none when no cut
-// pays.
-std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles) {
+// remaining tiles go back into the queue as a later item.  Both parts of a
+// cut keep at least kMinBalancePiece tiles (every piece costs a set-up, and
+// its rows a merge).  Returns each item's interior cut points (tile indices,
+// ascending); none when no cut pays.
+std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles, int n_units) {
   std::vector<std::vector<int32_t>> cuts(tiles.size());
   struct Seg {
     int64_t len;
@@ -185,11 +187,11 @@ std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles
       lens.push_back(tiles[i]);
     }
   if (lens.empty()) return cuts;
-  const int64_t ideal = (total + kComputeUnits - 1) / kComputeUnits;
+  const int64_t ideal = (total + n_units - 1) / n_units;
   const int64_t limit = (int64_t)(ideal * kBalanceSlack);
   // The schedule without cuts.
   std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
-  for (int u = 0; u < kComputeUnits; ++u) units.push(0);
+  for (int u = 0; u < n_units; ++u) units.push(0);
   int64_t makespan = 0;
   for (int64_t len : lens) {
     const int64_t t = units.top() + len + kItemSetupTiles;
@@ -200,7 +202,7 @@ std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles
   if (makespan <= limit) return cuts;
   // The same schedule with cuts.
   while (!units.empty()) units.pop();
-  for (int u = 0; u < kComputeUnits; ++u) units.push(0);
+  for (int u = 0; u < n_units; ++u) units.push(0);
   for (size_t i = 0; i < tiles.size(); ++i)
     if (tiles[i] > 0) queue.push(Seg{tiles[i], (int32_t)i, 0});
   while (!queue.empty()) {
@@ -210,11 +212,10 @@ std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles
     units.pop();
     int64_t take = s.len;
     if (load + s.len + kItemSetupTiles > limit && (int64_t)cuts[s.item].size() + 1 < kMaxPieces) {
-      // Fill this unit up to the ideal; both parts keep at least
-      // kMinPieceTiles tiles.
-      int64_t room = ideal - load - kItemSetupTiles;
-      room = std::min(room, s.len - kMinPieceTiles);
-      if (room >= kMinPieceTiles) take = room;
+      // Fill this unit up to the ideal, or give it the smallest piece when
+      // it is there already.
+      const int64_t room = ideal - load - kItemSetupTiles;
+      if (s.len >= 2 * kMinBalancePiece) take = std::min(std::max(room, kMinBalancePiece), s.len - kMinBalancePiece);
     }
     units.push(load + take + kItemSetupTiles);
     if (take < s.len) {
@@ -307,10 +308,20 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
         for (int64_t k = 1; k < n; ++k) cuts[bi * n_groups + g].push_back((int32_t)(blocks[bi].tiles * k / n));
     }
   } else if (target_pieces > 0) {
-    std::vector<int64_t> tiles(blocks.size() * n_groups);
-    for (size_t bi = 0; bi < blocks.size(); ++bi)
-      for (int g = 0; g < n_groups; ++g) tiles[bi * n_groups + g] = blocks[bi].tiles;
-    cuts = balance_cuts(tiles);
+    // With the head groups a multiple of the XCDs, each XCD's list is its own
+    // schedule on its 32 compute units; otherwise the lists share the units
+    // (the interleave below moves items between XCDs) and one schedule over
+    // all of them is the closer model.
+    const int n_sched = n_groups % kXcds == 0 ? kXcds : 1;
+    cuts.resize(blocks.size() * n_groups);
+    for (int x = 0; x < n_sched; ++x) {
+      std::vector<int64_t> tiles(blocks.size() * n_groups, 0);
+      for (size_t bi = 0; bi < blocks.size(); ++bi)
+        for (int g = x; g < n_groups; g += n_sched) tiles[bi * n_groups + g] = blocks[bi].tiles;
+      const std::vector<std::vector<int32_t>> c = balance_cuts(tiles, kComputeUnits / n_sched);
+      for (size_t i = 0; i < c.size(); ++i)
+        if (!c[i].empty()) cuts[i] = c[i];
+    }
   }
   out->splits.clear();
   out->n_pieces = 0;
