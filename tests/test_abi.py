@@ -286,10 +286,10 @@ def test_workspace_holds_piece_slots_for_split_walks():
     split = cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8)
     assert 16 * 62 * piece <= split < 16 * 62 * piece + (1 << 20)
     # The 32K Llama-3-8B rank-0 shard: 688 items of 96 positions x 4 heads,
-    # 344 of them long (chunk 7); 88 of those are cut in three, so that each
-    # compute unit ends near the ideal.
+    # 344 of them long (chunk 7), 43 for each XCD's 32 compute units; 11 of
+    # each XCD's are cut in two, so that every unit ends near the ideal.
     balanced = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
-    assert 264 * piece <= balanced < 264 * piece + (1 << 20)
+    assert 176 * piece <= balanced < 176 * piece + (1 << 20)
     # The 70B shard's eight pass-KV partials: 21888 items of 32 bytes and
     # the descriptors, no pieces.
     many = cp.workspace_size([_desc(R=131072, C=8, kv_rank=s) for s in range(8)], 64, 8)
