@@ -196,10 +196,12 @@ typedef struct cp_partial_desc {
  * Device workspace bytes cp_attn_partial needs for this descriptor set: the
  * device copy of the descriptors and the scheduled work list, and, when the
  * set has few work items with long key walks (a short suffix over a long
- * cached prefix), one slot of 256 x (128 + 1) fp32 per piece the walks are
- * split into (about a thousand pieces at most).  Deterministic in the
- * descriptors and head counts.  0 on invalid arguments (and cp_last_error
- * says why).
+ * cached prefix) or long items that do not divide evenly among the compute
+ * units, one slot of rows x (128 + 1) fp32 per piece the walks are split
+ * into (rows = 256 or 384, the launch's workgroup size; about a thousand
+ * pieces at most).  Deterministic in the descriptors, the head counts and
+ * the cp_set_workgroup_rows setting.  0 on invalid arguments (and
+ * cp_last_error says why).
  */
 size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_descs,
                                       int32_t n_heads_q, int32_t n_heads_kv);
@@ -232,6 +234,21 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
 int cp_attn_partial(const cp_partial_desc* descs, int32_t n_descs, int32_t n_heads_q,
                     int32_t n_heads_kv, int32_t head_dim, float softmax_scale,
                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Tuning control of cp_attn_partial's work decomposition (a library
+ * interface, not from the paper).  Each launch runs workgroups of 256 or
+ * 384 (query, head) rows -- 8 waves of two or three 16-row blocks; the
+ * larger shares each K/V tile between more rows, the smaller fills the
+ * compute units better when the launch has few or evenly long work items --
+ * and by default (rows = 0) the host plan picks the one whose simulated
+ * schedule ends first.  rows = 256 or 384 pins that shape for every later
+ * call in the process (reproducible timings, tests of each kernel shape);
+ * results agree within rounding either way.  Process-wide; takes effect at
+ * the next call.
+ * Errors: CP_ERR_INVALID for any other value.
+ */
+int cp_set_workgroup_rows(int32_t rows);
 
 /*
  * cp_attn_partial for callers that cannot allocate: code under HIP graph

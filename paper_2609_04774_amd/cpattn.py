@@ -33,7 +33,8 @@ CP_MAX_DEGREE = 64
 CP_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 EXPORTED = ("cp_status_string", "cp_last_error", "cp_shard_plan", "cp_shard_inverse",
-            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_attn_partial_noalloc", "cp_attn_merge",
+            "cp_attn_partial_workspace_size", "cp_attn_partial", "cp_set_workgroup_rows",
+            "cp_attn_partial_noalloc", "cp_attn_merge",
             "cp_kv_writeback", "cp_repartition", "cp_repartition_all", "cp_kv_gather")
 
 
@@ -102,6 +103,8 @@ def _load():
     lib.cp_attn_partial.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.cp_set_workgroup_rows.restype = ctypes.c_int
+    lib.cp_set_workgroup_rows.argtypes = [ctypes.c_int32]
     lib.cp_attn_partial_noalloc.restype = ctypes.c_int
     lib.cp_attn_partial_noalloc.argtypes = [ctypes.POINTER(CpPartialDesc), ctypes.c_int32, ctypes.c_int32,
                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p]
@@ -311,6 +314,12 @@ def attn_partial(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int
     _check(lib.cp_attn_partial(arr, len(descs), n_heads_q, n_heads_kv, head_dim,
                                float(softmax_scale), _ptr(workspace), nbytes,
                                _stream_handle(stream)))
+
+
+def set_workgroup_rows(rows: int) -> None:
+    """cp_set_workgroup_rows: 0 lets each launch choose its workgroup size
+    (256 or 384 rows); 256 or 384 pins it for the process."""
+    _check(lib.cp_set_workgroup_rows(int(rows)))
 
 
 def attn_partial_noalloc(descs: Sequence[CpPartialDesc], n_heads_q: int, n_heads_kv: int,

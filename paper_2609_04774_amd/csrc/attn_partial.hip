@@ -60,8 +60,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;                    // wave64s per workgroup, two per SIMD
-constexpr int kNB = 3;                       // blocks of 16 rows per wave
-constexpr int kBlockRows = 16;
+constexpr int kBlockRows = 16;               // a wave holds NB (2 or 3) blocks of 16 query rows
 constexpr int kTileKeys = 32;
 constexpr int kBufs = 8;                     // LDS tile buffers, each for K and for V
 constexpr int kAhead = 5;                    // the iteration of tile j loads tile j + kAhead
@@ -340,64 +339,70 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 
 // Scores of one tile: s[kb][b] = S^T of key half kb and query block b;
 // register r of it is key 16kb + 4g + r of the tile.
-typedef f32x4 Scores[2][kNB];
+template <int NB>
+using Scores = f32x4[2][NB];
 
 // One step of S^T = K Q^T (K fragment q = 2ds + kb) for the three blocks.
 // Every operand lives in VGPRs, and the compiler sees the instructions, so
 // it keeps the matrix-core hazards (result reads, operand overwrites) itself.
-__device__ __forceinline__ void qk_step(Scores& s, const bf16x8& k, const bf16x8 (&qf)[kNB][4], int q) {
+template <int NB>
+__device__ __forceinline__ void qk_step(Scores<NB>& s, const bf16x8& k, const bf16x8 (&qf)[NB][4], int q) {
   const int kb = q & 1, ds = q >> 1;
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) s[kb][b] = mfma16(k, qf[b][ds], ds == 0 ? f32x4{} : s[kb][b]);
+  for (int b = 0; b < NB; ++b) s[kb][b] = mfma16(k, qf[b][ds], ds == 0 ? f32x4{} : s[kb][b]);
 }
 
 // S^T = K Q^T for one 32-key tile (the prologue's first tile, and redos).
-__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[kNB][4],
-                                        Scores& s) {
+template <int NB>
+__device__ __forceinline__ void qk_tile(const unsigned char* sk, const FragOffsets& fo, const bf16x8 (&qf)[NB][4],
+                                        Scores<NB>& s) {
 #pragma unroll
   for (int q = 0; q < 8; ++q) qk_step(s, *reinterpret_cast<const bf16x8*>(k_frag_addr(sk, fo, q)), qf, q);
 }
 
 // O^T += V^T P^T for one 32-key tile (the last one), with the bf16 row sums.
-__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[kNB],
-                                        f32x4 (&o)[8][kNB], const bf16x8& ones, f32x4 (&psum)[kNB]) {
+template <int NB>
+__device__ __forceinline__ void pv_tile(const unsigned char* sv, const FragOffsets& fo, const bf16x8 (&pf)[NB],
+                                        f32x4 (&o)[8][NB], const bf16x8& ones, f32x4 (&psum)[NB]) {
 #pragma unroll
   for (int db = 0; db < 8; ++db) {
     const bf16x8 vf = v_frag(sv, fo, db);
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) o[db][b] = mfma16(vf, pf[b], o[db][b]);
+    for (int b = 0; b < NB; ++b) o[db][b] = mfma16(vf, pf[b], o[db][b]);
   }
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) psum[b] = mfma16(ones, pf[b], psum[b]);
+  for (int b = 0; b < NB; ++b) psum[b] = mfma16(ones, pf[b], psum[b]);
 }
 
 // Masks keys at tile offsets >= lim[b]; register r of s[kb][b] is tile key
 // 16kb + 4g + r.
-__device__ __forceinline__ void mask_tile(Scores& s, int g, const int (&lim)[kNB]) {
+template <int NB>
+__device__ __forceinline__ void mask_tile(Scores<NB>& s, int g, const int (&lim)[NB]) {
   // Compare the constant part of the offset with lim - 4g, so that no
   // per-register offsets need to be kept in registers.
-  int limg[kNB];
+  int limg[NB];
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) limg[b] = lim[b] - 4 * g;
+  for (int b = 0; b < NB; ++b) limg[b] = lim[b] - 4 * g;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
-      for (int b = 0; b < kNB; ++b)
+      for (int b = 0; b < NB; ++b)
         if (16 * kb + r >= limg[b]) s[kb][b][r] = -INFINITY;
 }
 
 // Keys at tile offsets >= lim are past the range end (hi) or after the
 // lane's query (position q0 + qrel).  A tile past the wave's last query is
 // masked entirely.
+template <int NB>
 __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_active, int wave_hi,
-                                            const int (&qrel)[kNB], const bool (&valid)[kNB], int (&lim)[kNB]) {
+                                            const int (&qrel)[NB], const bool (&valid)[NB], int (&lim)[NB]) {
   const bool live = wave_active && x.t0 <= wave_hi;
   const int a = q0 + 1 - x.t0;
   const int h = x.hi - x.t0;
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
+  for (int b = 0; b < NB; ++b) {
     int e = qrel[b] + a < h ? qrel[b] + a : h;
     e = e < 0 ? 0 : (e > kTileKeys ? kTileKeys : e);
     lim[b] = (live && valid[b]) ? e : 0;
@@ -423,7 +428,6 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 // against the running max (see kMaxTileSum).  The overflow check, and the
 // exact redo of a tile in the rare case that it fails, follow the region.
 constexpr int kSlots = 16;
-constexpr int kUnits = 36;
 constexpr int kLookahead = 2;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
@@ -434,9 +438,10 @@ __device__ __forceinline__ void pin(const T& x) {
   asm volatile("" ::"v"(x));
 }
 
+template <int NB>
 struct SoftmaxState {
-  float rs[kNB];      // fp32 sum of this tile's probabilities, per block
-  bf16x2 pp[kNB][4];  // bf16 pairs: [half 0 regs 0-1, 2-3, half 1 regs 0-1, 2-3]
+  float rs[NB];      // fp32 sum of this tile's probabilities, per block
+  bf16x2 pp[NB][4];  // bf16 pairs: [half 0 regs 0-1, 2-3, half 1 regs 0-1, 2-3]
 };
 
 // Pair t of block b's 8 scores (t = 2 kb + r/2, registers r, r+1 of half
@@ -445,7 +450,8 @@ struct SoftmaxState {
 // bf16-rounded values, which normalises O, is taken by an MFMA over the P
 // fragments (psum in the kernel): a dot-product instruction here would share
 // the matrix pipes with the tile's MFMAs and cost far more issue time.
-__device__ __forceinline__ void pack_and_sum(int b, int t, const Scores& s, SoftmaxState& st) {
+template <int NB>
+__device__ __forceinline__ void pack_and_sum(int b, int t, const Scores<NB>& s, SoftmaxState<NB>& st) {
   const int kb = t >> 1, r = 2 * (t & 1);
   const bf16x2 pp = bf16x2{(__bf16)s[kb][b][r], (__bf16)s[kb][b][r + 1]};
   st.pp[b][t] = pp;
@@ -459,7 +465,8 @@ __device__ __forceinline__ void pack_and_sum(int b, int t, const Scores& s, Soft
 
 // Unit u: pair t = (u / 3) % 4 of block b = u / 12; kind u % 3 (0, 1: one
 // exponential each; 2: pack and sum).
-__device__ __forceinline__ void softmax_unit(int u, Scores& s, SoftmaxState& st, const float (&m_run)[kNB],
+template <int NB>
+__device__ __forceinline__ void softmax_unit(int u, Scores<NB>& s, SoftmaxState<NB>& st, const float (&m_run)[NB],
                                              float sl2) {
   const int b = u / 12, t = (u / 3) % 4, kind = u % 3;
   if (kind < 2) {
@@ -474,7 +481,8 @@ __device__ __forceinline__ void softmax_unit(int u, Scores& s, SoftmaxState& st,
 
 // Max of block b's scores of one query (a lane's 8 and the three other
 // lanes' 24), in exponent units.
-__device__ __forceinline__ float tile_max(const Scores& s, int b, float sl2) {
+template <int NB>
+__device__ __forceinline__ float tile_max(const Scores<NB>& s, int b, float sl2) {
   float mx = max3(__builtin_elementwise_maximum(s[0][b][0], s[0][b][1]), s[0][b][2], s[0][b][3]);
   mx = max3(max3(mx, s[1][b][0], s[1][b][1]), s[1][b][2], s[1][b][3]);
   return quad_max(mx) * sl2;
@@ -491,13 +499,14 @@ __device__ __forceinline__ bf16x8 load_frag(int g, const unsigned char* sv, cons
 // s_in: S_j (masked), turned into its probabilities against m_run (their
 // bf16 pairs and sums in st); s_out: receives S_{j+1}.  pf: P_{j-1}, added
 // into O.
+template <int NB>
 __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const unsigned char* sk,
                                                  const unsigned char* sv_next, const FragOffsets& fo,
-                                                 const bf16x8 (&qf)[kNB][4], const bf16x8 (&pf)[kNB],
-                                                 f32x4 (&o)[8][kNB], Scores& s_in, Scores& s_out,
-                                                 const float (&m_run)[kNB], float sl2, const TileLoad& ld,
-                                                 SoftmaxState& st, bf16x8 (&pre)[kLookahead], const bf16x8& ones,
-                                                 f32x4 (&psum)[kNB]) {
+                                                 const bf16x8 (&qf)[NB][4], const bf16x8 (&pf)[NB],
+                                                 f32x4 (&o)[8][NB], Scores<NB>& s_in, Scores<NB>& s_out,
+                                                 const float (&m_run)[NB], float sl2, const TileLoad& ld,
+                                                 SoftmaxState<NB>& st, bf16x8 (&pre)[kLookahead], const bf16x8& ones,
+                                                 f32x4 (&psum)[NB]) {
   bf16x8 fr[16];
 #pragma unroll
   for (int g = 0; g < kLookahead; ++g) fr[g] = pre[g];
@@ -511,8 +520,8 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
     if ((slot & 7) == 1) issue_load(ld, slot >> 3);
     if (slot < 8) {
 #pragma unroll
-      for (int b = 0; b < kNB; ++b) o[slot][b] = mfma16(fr[slot], pf[b], o[slot][b]);
-      if (slot >= 2 && (slot & 1) == 0 && (slot - 2) / 2 < kNB) {
+      for (int b = 0; b < NB; ++b) o[slot][b] = mfma16(fr[slot], pf[b], o[slot][b]);
+      if (slot >= 2 && (slot & 1) == 0 && (slot - 2) / 2 < NB) {
         const int b = (slot - 2) / 2;
         psum[b] = mfma16(ones, pf[b], psum[b]);
       }
@@ -520,7 +529,7 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
       qk_step(s_out, fr[slot], qf, slot - 8);
     }
 #pragma unroll
-    for (int u = (slot * kUnits) / kSlots; u < ((slot + 1) * kUnits) / kSlots; ++u)
+    for (int u = (slot * 12 * NB) / kSlots; u < ((slot + 1) * 12 * NB) / kSlots; ++u)
       softmax_unit(u, s_in, st, m_run, sl2);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -532,10 +541,11 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
 // 2^(m_old - m_new) (exactly 1 where it did not move, 0 before a query's
 // first visible key), and the tile's probabilities are taken against the
 // new max.
-__device__ __forceinline__ void exact_softmax(Scores& s, float (&m_run)[kNB], float (&l_run)[kNB],
-                                              f32x4 (&psum)[kNB], f32x4 (&o)[8][kNB], float sl2, SoftmaxState& st) {
+template <int NB>
+__device__ __forceinline__ void exact_softmax(Scores<NB>& s, float (&m_run)[NB], float (&l_run)[NB],
+                                              f32x4 (&psum)[NB], f32x4 (&o)[8][NB], float sl2, SoftmaxState<NB>& st) {
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
+  for (int b = 0; b < NB; ++b) {
     const float m_new = __builtin_elementwise_maximum(tile_max(s, b, sl2), m_run[b]);
     const float alpha = __builtin_amdgcn_exp2f(m_run[b] - m_new);
     l_run[b] *= alpha;
@@ -545,7 +555,7 @@ __device__ __forceinline__ void exact_softmax(Scores& s, float (&m_run)[kNB], fl
     m_run[b] = m_new;
   }
 #pragma unroll
-  for (int b = 0; b < kNB; ++b)
+  for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -563,6 +573,7 @@ __device__ __forceinline__ void exact_softmax(Scores& s, float (&m_run)[kNB], fl
 constexpr int kLoadsPerTile = 2;  // K and V loads of one tile per wave
 constexpr int kWaitVm(int n) { return 0x0F70 | n; }
 
+template <int NB>
 __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevDesc* __restrict__ descs,
                                                                      const WorkItem* __restrict__ items,
                                                                      PartialParams p) {
@@ -592,13 +603,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   const int wg_last = (qb0 + p.q_per_wg < q_len ? qb0 + p.q_per_wg : q_len) - 1;
   const int wg_pos_hi = q_begin + wg_last;
 
-  int head_b[kNB];
-  int qrel_b[kNB];  // query index relative to the workgroup's first query
-  bool valid_b[kNB];
+  int head_b[NB];
+  int qrel_b[NB];  // query index relative to the workgroup's first query
+  bool valid_b[NB];
   int wave_lo = INT32_MAX, wave_hi = -1;
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
-    const int bi = kNB * wave + b;
+  for (int b = 0; b < NB; ++b) {
+    const int bi = NB * wave + b;
     head_b[b] = head0 + bi / qblocks_per_head;
     const int qo = (bi % qblocks_per_head) * kBlockRows;
     qrel_b[b] = qo + l16;
@@ -639,7 +650,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // workgroup takes this exit together (n_tiles is the workgroup's).
   if (n_tiles == 0) {
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) {
+    for (int b = 0; b < NB; ++b) {
       if (!valid_b[b]) continue;
       const int64_t row = ooff + qb0 + qrel_b[b];
       float* orow = d.o + (row * Hq + head_b[b]) * kHeadDim;
@@ -702,9 +713,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // lane 16g + i holds 8 consecutive head-dim values (8g .. 8g+7 of step ds)
   // of query i of each block, for each of the 4 steps of 32 along D.  Rows
   // past the chunk's end are zero and masked out of every tile.
-  bf16x8 qf[kNB][4];
+  bf16x8 qf[NB][4];
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
+  for (int b = 0; b < NB; ++b) {
     const int64_t qrow_i = loff + (valid_b[b] ? qb0 + qrel_b[b] : qb0);
     const __attribute__((address_space(1))) bf16x8* qrow =
         (const __attribute__((address_space(1))) bf16x8*)(d.q + (qrow_i * Hq + head_b[b]) * kHeadDim + g4 * 8);
@@ -748,20 +759,20 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
 
   const FragOffsets fo = frag_offsets(lane);
   const float sl2 = p.scale_log2;
-  f32x4 o[8][kNB];
-  float m_run[kNB];                            // running max (exponent units)
-  float l_run[kNB];                            // sum of the fp32 probabilities (lane's keys)
+  f32x4 o[8][NB];
+  float m_run[NB];                            // running max (exponent units)
+  float l_run[NB];                            // sum of the fp32 probabilities (lane's keys)
   // Sums of the bf16-rounded probabilities, by a 16x16x32 MFMA with an
   // all-ones A over each block's P fragment: every row of psum[b] holds the
   // sum over the tile's 32 keys of the lane's query, so every lane has its
   // query's full sum.
-  f32x4 psum[kNB];
+  f32x4 psum[NB];
   bf16x8 ones;
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
-  bf16x8 pf[kNB];                              // P of the previous tile
+  bf16x8 pf[NB];                              // P of the previous tile
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
+  for (int b = 0; b < NB; ++b) {
 #pragma unroll
     for (int db = 0; db < 8; ++db) o[db][b] = f32x4{};
     m_run[b] = kNoMax;
@@ -770,7 +781,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     pf[b] = bf16x8{};
   }
   // Scores of the current tile alternate between two register sets.
-  Scores sa, sb;
+  Scores<NB> sa, sb;
   const int q0 = q_begin + qb0;
 
   // The first iteration's P V step reads the V buffer before the first
@@ -785,9 +796,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   auto masked_tile = [&](int j) {
     return (j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c;
   };
-  auto mask_if_needed = [&](int j, Scores& s) {
+  auto mask_if_needed = [&](int j, Scores<NB>& s) {
     if (masked_tile(j)) {
-      int lim[kNB];
+      int lim[NB];
       tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
       mask_tile(s, g4, lim);
     }
@@ -802,7 +813,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     qk_tile(smem + (t_first & (kBufs - 1)) * kTileBytes, fo, qf, sa);
     mask_if_needed(t_first, sa);
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) m_run[b] = __builtin_elementwise_maximum(tile_max(sa, b, sl2), kNoMax);
+    for (int b = 0; b < NB; ++b) m_run[b] = __builtin_elementwise_maximum(tile_max(sa, b, sl2), kNoMax);
   }
 
   // Iteration j (tile buffer B = j % kBufs): mask
@@ -828,24 +839,26 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     cur = ld;
     return ld;
   };
-  auto iteration = [&](int j, Scores& s_in, Scores& s_out) {
+  auto iteration = [&](int j, Scores<NB>& s_in, Scores<NB>& s_out) {
     const int B = j & (kBufs - 1);
     mask_if_needed(j, s_in);
     const TileLoad ld = next_load(j);
-    SoftmaxState st;
+    SoftmaxState<NB> st;
     pipelined_region(smem + ((B + kBufs - 1) % kBufs) * kTileBytes, smem + ((B + 1) % kBufs) * kTileBytes,
                      smem + B * kTileBytes, fo, qf, pf, o, s_in, s_out, m_run, sl2, ld, st, pre, ones, psum);
     // Rare: some lane's probabilities were too large (its max grew by more
     // than ~2^13, or it saw its first key).  Redo the tile exactly; its K
     // tile is still in buffer B (tile j + 8 is loaded three iterations on).
-    const bool ok = st.rs[0] <= kMaxTileSum && st.rs[1] <= kMaxTileSum && st.rs[2] <= kMaxTileSum;
+    bool ok = true;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) ok = ok && st.rs[b] <= kMaxTileSum;
     if (__builtin_amdgcn_ballot_w64(!ok) != 0) {
       qk_tile(smem + B * kTileBytes, fo, qf, s_in);
       mask_if_needed(j, s_in);
       exact_softmax(s_in, m_run, l_run, psum, o, sl2, st);
     }
 #pragma unroll
-    for (int b = 0; b < kNB; ++b) {
+    for (int b = 0; b < NB; ++b) {
       l_run[b] += st.rs[b];
       pf[b] = __builtin_shufflevector(__builtin_shufflevector(st.pp[b][0], st.pp[b][1], 0, 1, 2, 3),
                                       __builtin_shufflevector(st.pp[b][2], st.pp[b][3], 0, 1, 2, 3), 0, 1, 2, 3,
@@ -885,7 +898,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   // Normalise and store: O^T register r of (db, b) is head-dim 16db + 4g + r
   // of this lane's query of block b.
 #pragma unroll
-  for (int b = 0; b < kNB; ++b) {
+  for (int b = 0; b < NB; ++b) {
     const float lt = quad_sum(l_run[b]);
     const float ltb = psum[b][0];
     const bool live = (m_run[b] > 0.5f * kNoMax) && (lt > 0.f) && (ltb > 0.f);
@@ -896,10 +909,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     if (it.piece >= 0) {
       // One piece of a split walk: its partial over its keys goes to the
       // piece slot (row 16 * block + query of the work item).
-      unsigned char* slot = p.pieces + (size_t)it.piece * kPieceBytes;
-      const int r = (kNB * wave + b) * kBlockRows + l16;
+      unsigned char* slot = p.pieces + (size_t)it.piece * piece_bytes(kWaves * kBlockRows * NB);
+      const int r = (NB * wave + b) * kBlockRows + l16;
       orow = reinterpret_cast<float*>(slot) + (size_t)r * kHeadDim;
-      lrow = reinterpret_cast<float*>(slot + kPieceOBytes) + r;
+      lrow = reinterpret_cast<float*>(slot + piece_o_bytes(kWaves * kBlockRows * NB)) + r;
     } else {
       if (!valid_b[b]) continue;
       const int64_t row = ooff + qb0 + qrel_b[b];
@@ -924,12 +937,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
 // a piece with LSE_k = -inf weighing 0 (and not read).  Each row of the item
 // is written to the descriptor's output where the unsplit item would have
 // written it.  32 lanes per row (float4 each), 8 rows per 256-thread block,
-// kRowsPerWG / 8 blocks per split item.
+// rows_per_wg / 8 blocks per split item.
 constexpr int kMergeRowsPerBlock = 8;
 
 __global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restrict__ descs,
                                                           const SplitItem* __restrict__ splits, PartialParams p) {
-  const int blocks_per_item = kRowsPerWG / kMergeRowsPerBlock;
+  const int blocks_per_item = p.rows_per_wg / kMergeRowsPerBlock;
+  const size_t slot_bytes = piece_bytes(p.rows_per_wg), o_bytes = piece_o_bytes(p.rows_per_wg);
   const SplitItem sp = splits[blockIdx.x / blocks_per_item];
   const int r = (blockIdx.x % blocks_per_item) * kMergeRowsPerBlock + (threadIdx.x >> 5);
   const int lane = threadIdx.x & 31;
@@ -947,16 +961,16 @@ __global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restr
 
   float m = -INFINITY;
   for (int k = 0; k < sp.n_pieces; ++k) {
-    const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * kPieceBytes;
-    m = fmaxf(m, reinterpret_cast<const float*>(slot + kPieceOBytes)[r]);
+    const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * slot_bytes;
+    m = fmaxf(m, reinterpret_cast<const float*>(slot + o_bytes)[r]);
   }
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float lse = -INFINITY;
   if (m != -INFINITY) {
     float total = 0.f;
     for (int k = 0; k < sp.n_pieces; ++k) {
-      const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * kPieceBytes;
-      const float lk = reinterpret_cast<const float*>(slot + kPieceOBytes)[r];
+      const unsigned char* slot = p.pieces + (size_t)(sp.first_piece + k) * slot_bytes;
+      const float lk = reinterpret_cast<const float*>(slot + o_bytes)[r];
       if (lk == -INFINITY) continue;
       const float w = expf(lk - m);
       total += w;
@@ -981,12 +995,18 @@ __global__ __launch_bounds__(256) void split_merge_kernel(const DevDesc* __restr
 
 int launch_partial(const PartialParams& p, void* stream) {
   if (p.n_items == 0) return CP_OK;
-  hipLaunchKernelGGL(attn_partial_kernel, dim3((unsigned)p.n_items), dim3(64 * kWaves), 0, (hipStream_t)stream,
-                     p.descs, p.items, p);
+  if (p.rows_per_wg == kWaves * kBlockRows * 3)
+    hipLaunchKernelGGL(attn_partial_kernel<3>, dim3((unsigned)p.n_items), dim3(64 * kWaves), 0, (hipStream_t)stream,
+                       p.descs, p.items, p);
+  else if (p.rows_per_wg == kWaves * kBlockRows * 2)
+    hipLaunchKernelGGL(attn_partial_kernel<2>, dim3((unsigned)p.n_items), dim3(64 * kWaves), 0, (hipStream_t)stream,
+                       p.descs, p.items, p);
+  else
+    return fail(CP_ERR_INVALID, "cp_attn_partial: unsupported workgroup shape");
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial launch: ") + hipGetErrorString(e));
   if (p.n_splits > 0) {
-    const unsigned blocks = (unsigned)p.n_splits * (unsigned)(kRowsPerWG / kMergeRowsPerBlock);
+    const unsigned blocks = (unsigned)p.n_splits * (unsigned)(p.rows_per_wg / kMergeRowsPerBlock);
     hipLaunchKernelGGL(split_merge_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, p.descs, p.splits, p);
     e = hipGetLastError();
     if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("cp_attn_partial merge launch: ") + hipGetErrorString(e));

@@ -22,6 +22,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <numeric>
 #include <queue>
@@ -48,11 +49,12 @@ int gcd_int(int a, int b) {
   return a;
 }
 
-Shape shape_for(int Hq, int Hkv) {
+Shape shape_for(int Hq, int Hkv, int rows) {
   const int G = Hq / Hkv;
   Shape s;
+  s.rows_per_wg = rows;
   s.heads_per_wg = gcd_int(G, 8);
-  s.q_per_wg = kRowsPerWG / s.heads_per_wg;
+  s.q_per_wg = rows / s.heads_per_wg;
   s.groups_per_kv = G / s.heads_per_wg;
   return s;
 }
@@ -249,23 +251,13 @@ int64_t item_keys(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
   return keys;
 }
 
-}  // namespace
 
-namespace cpattn {
-
-int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
-               Plan* out) {
-  int st = check_heads(Hq, Hkv, "cp_attn_partial");
-  if (st != CP_OK) return st;
-  if (n_descs < 0) return fail(CP_ERR_INVALID, "cp_attn_partial: n_descs < 0");
-  if (n_descs > 0 && !descs) return fail(CP_ERR_INVALID, "cp_attn_partial: descs is NULL");
-  out->shape = shape_for(Hq, Hkv);
+// The work list of one launch for one workgroup shape: items, split items and
+// piece count into *out (whose descriptors are set).
+int plan_items(int32_t Hq, int32_t Hkv, int rows, int64_t target_pieces, Plan* out) {
+  out->shape = shape_for(Hq, Hkv, rows);
   const Shape& sh = out->shape;
-  out->descs.resize(n_descs);
-  for (int i = 0; i < n_descs; ++i) {
-    st = to_dev(descs[i], i, &out->descs[i]);
-    if (st != CP_OK) return st;
-  }
+  const int n_descs = (int)out->descs.size();
   const int n_groups = Hkv * sh.groups_per_kv;
   struct Cand {
     int64_t cost;
@@ -369,6 +361,83 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   return CP_OK;
 }
 
+// Estimated time (microseconds) of a planned launch: the in-order dispatch
+// of its work list simulated on each XCD's 32 compute units (list item i on
+// XCD i % 8), an item taking its tiles times the shape's time per tile plus
+// a fixed set-up, then the split merge's traffic.  The 384-row shape's tile
+// is 1.5 times the 256-row one's work at kLargeTileGain times its rate (the
+// two kernels timed on launches that both balance).
+constexpr double kSmallTileUs = 0.93;   // a 256-row x 32-key tile on one compute unit
+constexpr double kLargeTileGain = 1.08;
+constexpr double kItemSetupUs = 4.0;
+constexpr double kMergeBytesPerUs = 5.0e6;
+
+double estimate_us(const Plan& plan) {
+  const double tile_us = plan.shape.rows_per_wg == kRowsLarge ? kSmallTileUs * 1.5 / kLargeTileGain : kSmallTileUs;
+  std::vector<std::priority_queue<double, std::vector<double>, std::greater<double>>> units(kXcds);
+  for (auto& q : units)
+    for (int u = 0; u < kComputeUnits / kXcds; ++u) q.push(0.0);
+  double makespan = 0.0;
+  for (size_t i = 0; i < plan.items.size(); ++i) {
+    const WorkItem& w = plan.items[i];
+    const int64_t tiles = w.t_end >= 0 ? (int64_t)(w.t_end - w.t_begin)
+                                       : item_tiles(plan.descs[w.desc], w.chunk, w.q_block, plan.shape.q_per_wg);
+    auto& q = units[i % kXcds];
+    const double t = q.top() + tiles * tile_us + kItemSetupUs;
+    q.pop();
+    q.push(t);
+    makespan = std::max(makespan, t);
+  }
+  if (plan.n_pieces) {
+    // Pieces written and read back, the merged rows written.
+    const double bytes = (double)piece_bytes(plan.shape.rows_per_wg) * (2.0 * plan.n_pieces + plan.splits.size());
+    makespan += bytes / kMergeBytesPerUs + kItemSetupUs;
+  }
+  return makespan;
+}
+
+// Work-group shape forced by cp_set_workgroup_rows (0: chosen per launch).
+std::atomic<int> g_forced_rows{0};
+
+}  // namespace
+
+extern "C" int cp_set_workgroup_rows(int32_t rows) {
+  if (rows != 0 && rows != kRowsSmall && rows != kRowsLarge)
+    return fail_static(CP_ERR_INVALID, "cp_set_workgroup_rows: rows must be 0, 256 or 384");
+  g_forced_rows.store(rows);
+  clear_error();
+  return CP_OK;
+}
+
+namespace cpattn {
+
+int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
+               Plan* out) {
+  int st = check_heads(Hq, Hkv, "cp_attn_partial");
+  if (st != CP_OK) return st;
+  if (n_descs < 0) return fail(CP_ERR_INVALID, "cp_attn_partial: n_descs < 0");
+  if (n_descs > 0 && !descs) return fail(CP_ERR_INVALID, "cp_attn_partial: descs is NULL");
+  out->descs.resize(n_descs);
+  for (int i = 0; i < n_descs; ++i) {
+    st = to_dev(descs[i], i, &out->descs[i]);
+    if (st != CP_OK) return st;
+  }
+  // The workgroup shape: two or three 16-row blocks per wave.  The larger
+  // shares every K/V fragment between more rows (faster per tile) but makes
+  // fewer, longer work items, which fill the compute units worse; plan both
+  // and keep the one whose simulated schedule ends first.
+  const int forced = g_forced_rows.load();
+  if (forced) return plan_items(Hq, Hkv, forced, target_pieces, out);
+  Plan small;
+  small.descs = out->descs;
+  st = plan_items(Hq, Hkv, kRowsSmall, target_pieces, &small);
+  if (st != CP_OK) return st;
+  st = plan_items(Hq, Hkv, kRowsLarge, target_pieces, out);
+  if (st != CP_OK) return st;
+  if (estimate_us(small) < estimate_us(*out)) *out = std::move(small);
+  return CP_OK;
+}
+
 static size_t align_up(size_t x) { return (x + kItemsAlign - 1) / kItemsAlign * kItemsAlign; }
 
 Layout layout_of(const Plan& plan) {
@@ -376,7 +445,7 @@ Layout layout_of(const Plan& plan) {
   l.items = align_up(plan.descs.size() * sizeof(DevDesc));
   l.splits = align_up(l.items + plan.items.size() * sizeof(WorkItem));
   l.pieces = align_up(l.splits + plan.splits.size() * sizeof(SplitItem));
-  l.total = l.pieces + (size_t)plan.n_pieces * kPieceBytes;
+  l.total = l.pieces + (size_t)plan.n_pieces * piece_bytes(plan.shape.rows_per_wg);
   return l;
 }
 
@@ -402,7 +471,7 @@ PartialParams partial_params(const Plan& plan, const Layout& lay, unsigned char*
   p.groups_per_kv = plan.shape.groups_per_kv;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.waves_per_wg = 8;
+  p.rows_per_wg = plan.shape.rows_per_wg;
   p.pieces = plan.n_pieces ? ws + lay.pieces : nullptr;
   p.splits = reinterpret_cast<const SplitItem*>(ws + lay.splits);
   p.n_splits = (int32_t)plan.splits.size();

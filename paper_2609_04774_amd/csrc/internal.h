@@ -43,7 +43,10 @@ bool plan_equal(const cp_rank_plan& a, const cp_rank_plan& b);
 
 constexpr int kHeadDim = 128;
 constexpr int kBlockTokens = 16;
-constexpr int kRowsPerWG = 384;      // (query, head) rows per workgroup
+// (query, head) rows per workgroup: 8 waves of 2 or 3 blocks of 16 rows,
+// chosen per launch by the host plan.
+constexpr int kRowsSmall = 256;
+constexpr int kRowsLarge = 384;
 
 // One descriptor as the kernel reads it.  Key sets are expressed as global
 // positions: the prefix [0, prefix_keys) through the block table, then up to
@@ -102,10 +105,10 @@ struct SplitItem {
   int32_t n_pieces;
 };
 
-// Workspace of one piece: fp32 O of the work item's 384 rows (row = 16 *
-// block + query), then their LSE.
-constexpr size_t kPieceOBytes = (size_t)kRowsPerWG * kHeadDim * 4;
-constexpr size_t kPieceBytes = kPieceOBytes + (size_t)kRowsPerWG * 4;
+// Workspace of one piece of a work item of `rows` rows: fp32 O of its rows
+// (row = 16 * block + query), then their LSE.
+__host__ __device__ constexpr size_t piece_o_bytes(int rows) { return (size_t)rows * kHeadDim * 4; }
+__host__ __device__ constexpr size_t piece_bytes(int rows) { return piece_o_bytes(rows) + (size_t)rows * 4; }
 
 struct PartialParams {
   const DevDesc* descs;
@@ -114,11 +117,11 @@ struct PartialParams {
   int32_t Hq;
   int32_t Hkv;
   int32_t heads_per_wg;   // query heads of one KV head handled by one workgroup
-  int32_t q_per_wg;       // query positions per workgroup (heads_per_wg * q_per_wg = 384)
+  int32_t q_per_wg;       // query positions per workgroup (heads_per_wg * q_per_wg = rows_per_wg)
   int32_t groups_per_kv;  // (Hq / Hkv) / heads_per_wg
   float scale_log2;       // softmax scale * log2(e)
   float scale;            // softmax scale
-  int32_t waves_per_wg;   // 8 (three 16-row blocks per wave)
+  int32_t rows_per_wg;    // 256 or 384 (8 waves of two or three 16-row blocks)
   unsigned char* pieces;  // piece slots (kPieceBytes each), or null when nothing is split
   const SplitItem* splits;
   int32_t n_splits;
@@ -130,7 +133,7 @@ int launch_partial(const PartialParams& p, void* stream);
 // entry points that take a caller workspace and the one that uses the
 // library's own scratch.
 struct Shape {
-  int heads_per_wg, q_per_wg, groups_per_kv;
+  int rows_per_wg, heads_per_wg, q_per_wg, groups_per_kv;
 };
 
 struct Plan {

@@ -274,26 +274,55 @@ def test_workspace_size_grows_with_work():
         cp.workspace_size([bad], 8, 2)
 
 
+def _piece(rows):
+    return rows * 128 * 4 + rows * 4
+
+
 def test_workspace_holds_piece_slots_for_split_walks():
     """Few query rows over a long cached prefix: the launch has few work items,
     so each item's key walk is split into pieces and the workspace grows by
-    one slot (fp32 O and LSE of 384 rows) per piece.  A launch whose long
-    items do not fill the 256 compute units evenly has some of them cut to
-    balance the schedule; one with many small items is never split."""
-    piece = 384 * 128 * 4 + 384 * 4
-    # 64 rows, 4 of 32 query heads per workgroup -> 16 items of 2049-2050
-    # tiles; about 1024 pieces in all: pieces of 33 tiles, 62 per item.
-    split = cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8)
-    assert 16 * 62 * piece <= split < 16 * 62 * piece + (1 << 20)
-    # The 32K Llama-3-8B rank-0 shard: 688 items of 96 positions x 4 heads,
-    # 344 of them long (chunk 7), 43 for each XCD's 32 compute units; 11 of
-    # each XCD's are cut in two, so that every unit ends near the ideal.
-    balanced = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
-    assert 176 * piece <= balanced < 176 * piece + (1 << 20)
-    # The 70B shard's eight pass-KV partials: 21888 items of 32 bytes and
-    # the descriptors, no pieces.
-    many = cp.workspace_size([_desc(R=131072, C=8, kv_rank=s) for s in range(8)], 64, 8)
-    assert 21888 * 32 <= many < 21888 * 32 + 8192
+    one slot (fp32 O and LSE of the workgroup's rows) per piece.  A launch
+    whose long items do not fill the 256 compute units evenly has some of
+    them cut to balance the schedule; one with many small items is never
+    split."""
+    try:
+        for rows in (256, 384):
+            cp.set_workgroup_rows(rows)
+            # 64 rows, 4 of 32 query heads per workgroup -> 16 items of
+            # 2049-2050 tiles; about 1024 pieces in all: pieces of 33 tiles, 62
+            # per item.
+            split = cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8)
+            assert 16 * 62 * _piece(rows) <= split < 16 * 62 * _piece(rows) + (1 << 20)
+        # The 32K Llama-3-8B rank-0 shard in 384-row workgroups: 688 items of
+        # 96 positions x 4 heads, 344 of them long (chunk 7), 43 for each
+        # XCD's 32 compute units; 11 of each XCD's are cut in two, so that
+        # every unit ends near the ideal.
+        cp.set_workgroup_rows(384)
+        balanced = cp.workspace_size([_desc(R=32768, C=4)], 32, 8)
+        assert 176 * _piece(384) <= balanced < 176 * _piece(384) + (1 << 20)
+        # The 70B shard's eight pass-KV partials: 21888 items of 32 bytes and
+        # the descriptors, no pieces.
+        many = cp.workspace_size([_desc(R=131072, C=8, kv_rank=s) for s in range(8)], 64, 8)
+        assert 21888 * 32 <= many < 21888 * 32 + 8192
+        # In 256-row workgroups the 32K shard's 512 long items fill two rounds
+        # exactly: nothing is cut.
+        cp.set_workgroup_rows(256)
+        assert cp.workspace_size([_desc(R=32768, C=4)], 32, 8) < _piece(256)
+        # Chosen per launch: the larger shape for the 32K rank-0 shard, the
+        # smaller for the few long walks (more, shorter pieces fill the units).
+        cp.set_workgroup_rows(0)
+        assert cp.workspace_size([_desc(R=32768, C=4)], 32, 8) == balanced
+        assert cp.workspace_size([_desc(P=65536, R=64, C=1)], 32, 8) < 16 * 62 * _piece(384)
+    finally:
+        cp.set_workgroup_rows(0)
+
+
+def test_workgroup_rows_setting():
+    for bad in (1, 128, 255, 512, -1):
+        with pytest.raises(cp.CpError):
+            cp.set_workgroup_rows(bad)
+    for ok in (256, 384, 0):
+        cp.set_workgroup_rows(ok)
 
 
 def _merge_status(n_parts=2, n_tokens=4, H=2, D=128, out=FAKE, lse_out=FAKE * 2, restore=None,

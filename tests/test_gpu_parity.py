@@ -22,6 +22,15 @@ from gpu_cases import Problem, compare, f64, DEV
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(autouse=True, params=[256, 384], ids=["rows256", "rows384"])
+def workgroup_rows(request):
+    """Every case runs on both attention kernel shapes (two or three 16-row
+    blocks per wave), pinned for the test and released after it."""
+    cp.set_workgroup_rows(request.param)
+    yield request.param
+    cp.set_workgroup_rows(0)
+
+
 def _restore_all_ranks(prob, kv_mode="allgather"):
     """Every rank's partial(s), merged and restored into original order by
     cp_attn_merge; returns (O [R, Hq, D], LSE [R, Hq]) on the GPU."""
