@@ -7,10 +7,13 @@
 //
 // How (FlashAttention-2 style online softmax, Dao 2023, with the running
 // max/sum recurrence of Milakov & Gimelshein 2018):
-//   * A workgroup of 8 wave64s (two per SIMD) owns 384 (query, head) rows
+//   * A workgroup of 8 wave64s (two per SIMD) owns 128 NB (query, head) rows
 //     that share one KV head: `heads_per_wg` query heads x `q_per_wg`
-//     consecutive positions.  Each wave owns three blocks of 16 rows, so
-//     every K and V fragment read from LDS feeds three MFMAs.  Two waves
+//     consecutive positions.  Each wave owns NB blocks of 16 rows, so every
+//     K and V fragment read from LDS feeds NB MFMAs.  The kernel comes in two
+//     shapes, NB = 3 (384 rows: fewer LDS bytes per FLOP) and NB = 2 (256
+//     rows: more, shorter work items); the host plan picks one per launch.
+//     Two waves
 //     per SIMD let one wave's vector and scalar work issue while the other's
 //     matrix work runs (a single wave issues one instruction at a time,
 //     whatever its type); the 256 registers per lane this leaves a wave hold
@@ -410,25 +413,27 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 }
 
 // One iteration's matrix and vector work as a fixed sequence of 16 slots,
-// each with one LDS fragment and three MFMAs (one per query block): slots
-// 0-7 add P_{j-1} V_{j-1} (V fragment = head-dim block slot), slots 8-15
-// compute S_{j+1} = K_{j+1} Q^T (K fragment slot - 8); slots 2, 4 and 6 also
-// take block (slot - 2)/2's bf16 row sums.  The softmax of S_j is cut into
-// units of roughly equal VALU time and dealt out over the slots, so that
-// every MFMA has vector work to overlap with.  LDS fragments are read two
-// slots ahead in one continuous stream: the last two slots read the next
-// iteration's first V fragments (of tile j, published since before this
-// pair of iterations), so no iteration starts by waiting for a fresh LDS
-// read.  The two loads of tile j+5 (K rows, then V rows) go out at slots 1
-// and 9.  Scheduling barriers keep the slots in this order.  The other wave
-// on the same SIMD runs the same sequence shifted in time, so one wave's
-// vector and scalar work issues while the other's matrix work runs.
+// each with one LDS fragment and NB MFMAs (one per query block): slots 0-7
+// add P_{j-1} V_{j-1} (V fragment = head-dim block slot), slots 8-15 compute
+// S_{j+1} = K_{j+1} Q^T (K fragment slot - 8); slots 2, 4 (and 6) also take
+// block (slot - 2)/2's bf16 row sums.  The softmax of S_j is cut into units
+// of roughly equal VALU time and dealt out over the slots, so that every
+// MFMA has vector work to overlap with.  LDS fragments are read a few slots
+// ahead (kLookahead: about 100 cycles of MFMA work) in one continuous stream:
+// the region's last slots read the next iteration's first V fragments (of
+// tile j, published since before this pair of iterations), so no iteration
+// starts by waiting for a fresh LDS read.  The two loads of tile j+5 (K rows,
+// then V rows) go out at slots 1 and 9.  Scheduling barriers keep the slots
+// in this order.  The other wave on the same SIMD runs the same sequence
+// shifted in time, so one wave's vector and scalar work issues while the
+// other's matrix work runs.
 //
-// Units: twelve times (two exponentials, one pack-and-sum) for score pairs,
+// Units: 4 NB times (two exponentials, one pack-and-sum) for score pairs,
 // against the running max (see kMaxTileSum).  The overflow check, and the
 // exact redo of a tile in the rare case that it fails, follow the region.
 constexpr int kSlots = 16;
-constexpr int kLookahead = 2;
+template <int NB>
+constexpr int kLookahead = NB == 2 ? 3 : 2;
 
 // Forces `x` to be computed before this point: an empty volatile asm that
 // reads it stays in program order with the scheduling barriers, so the
@@ -505,14 +510,14 @@ __device__ __forceinline__ void pipelined_region(const unsigned char* sv, const 
                                                  const bf16x8 (&qf)[NB][4], const bf16x8 (&pf)[NB],
                                                  f32x4 (&o)[8][NB], Scores<NB>& s_in, Scores<NB>& s_out,
                                                  const float (&m_run)[NB], float sl2, const TileLoad& ld,
-                                                 SoftmaxState<NB>& st, bf16x8 (&pre)[kLookahead], const bf16x8& ones,
+                                                 SoftmaxState<NB>& st, bf16x8 (&pre)[kLookahead<NB>], const bf16x8& ones,
                                                  f32x4 (&psum)[NB]) {
   bf16x8 fr[16];
 #pragma unroll
-  for (int g = 0; g < kLookahead; ++g) fr[g] = pre[g];
+  for (int g = 0; g < kLookahead<NB>; ++g) fr[g] = pre[g];
 #pragma unroll
   for (int slot = 0; slot < kSlots; ++slot) {
-    const int g = slot + kLookahead;
+    const int g = slot + kLookahead<NB>;
     if (g < 16)
       fr[g] = load_frag(g, sv, sk, fo);
     else
@@ -803,10 +808,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       mask_tile(s, g4, lim);
     }
   };
-  bf16x8 pre[kLookahead];
+  bf16x8 pre[kLookahead<NB>];
   if (n_tiles > 0 && wave_active) {
 #pragma unroll
-    for (int g = 0; g < kLookahead; ++g)
+    for (int g = 0; g < kLookahead<NB>; ++g)
       pre[g] = load_frag(g, smem + ((t_first + kBufs - 1) & (kBufs - 1)) * kTileBytes, smem, fo);
     // The first tile's scores, and the running max seeded with their max (so
     // that the first iteration's probabilities need no redo).
