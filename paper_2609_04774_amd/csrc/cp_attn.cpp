@@ -16,6 +16,10 @@
 // pieces in all; each piece is its own workgroup and writes a partial result
 // (O, LSE over its keys) to the workspace, and split_merge combines an item's
 // pieces exactly (the same log-sum-exp combination as cp_attn_merge).
+//
+// Workgroup shape.  The attention kernel runs 256- or 384-row workgroups; the
+// work list is built for both and the one whose simulated schedule ends first
+// is launched (balance cuts and the estimate below).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -250,7 +254,6 @@ int64_t item_keys(const DevDesc& d, int chunk, int64_t qb, int q_per_wg) {
   for (int s = 0; s < d.n_seg; ++s) keys += std::max<int64_t>(0, std::min(d.seg_hi[s], pos_hi + 1) - d.seg_lo[s]);
   return keys;
 }
-
 
 // The work list of one launch for one workgroup shape: items, split items and
 // piece count into *out (whose descriptors are set).
