@@ -345,7 +345,7 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 template <int NB>
 using Scores = f32x4[2][NB];
 
-// One step of S^T = K Q^T (K fragment q = 2ds + kb) for the three blocks.
+// One step of S^T = K Q^T (K fragment q = 2ds + kb) for the NB blocks.
 // Every operand lives in VGPRs, and the compiler sees the instructions, so
 // it keeps the matrix-core hazards (result reads, operand overwrites) itself.
 template <int NB>
