@@ -175,28 +175,37 @@ constexpr double kBalanceSlack = 1.03;
 // remaining tiles go back into the queue as a later item.  Both parts of a
 // cut keep at least kMinBalancePiece tiles (every piece costs a set-up, and
 // its rows a merge).  Returns each item's interior cut points (tile indices,
-// ascending); none when no cut pays.
-std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles, int n_units) {
-  std::vector<std::vector<int32_t>> cuts(tiles.size());
+// ascending) in `cuts` (indexed by the items' numbers, allocated only when a
+// cut is made); nothing when no cut pays.
+struct ItemTiles {
+  int64_t item;   // the item's number in the launch
+  int64_t tiles;  // its key walk
+};
+
+void balance_cuts(const std::vector<ItemTiles>& items, int n_units, size_t n_items_total,
+                  std::vector<std::vector<int32_t>>* cuts) {
   struct Seg {
     int64_t len;
-    int32_t item, t0;
+    int64_t item;
+    int32_t t0;
   };
-  auto longer = [](const Seg& a, const Seg& b) { return a.len < b.len || (a.len == b.len && a.item > b.item); };
-  std::priority_queue<Seg, std::vector<Seg>, decltype(longer)> queue(longer);
-  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
-  int64_t total = 0;
-  std::vector<int64_t> lens;
-  for (size_t i = 0; i < tiles.size(); ++i)
-    if (tiles[i] > 0) {
-      total += tiles[i] + kItemSetupTiles;
-      lens.push_back(tiles[i]);
-    }
-  if (lens.empty()) return cuts;
+  int64_t total = 0, longest = 0;
+  for (const ItemTiles& it : items) {
+    total += it.tiles + kItemSetupTiles;
+    longest = std::max(longest, it.tiles);
+  }
+  if (items.empty()) return;
   const int64_t ideal = (total + n_units - 1) / n_units;
   const int64_t limit = (int64_t)(ideal * kBalanceSlack);
+  // List scheduling ends within one item of the even spread: when the longest
+  // item fits in the slack, no schedule needs cuts (and none is simulated).
+  if (ideal + longest + kItemSetupTiles <= limit) return;
   // The schedule without cuts.
+  std::vector<int64_t> lens;
+  lens.reserve(items.size());
+  for (const ItemTiles& it : items) lens.push_back(it.tiles);
   std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
   for (int u = 0; u < n_units; ++u) units.push(0);
   int64_t makespan = 0;
   for (int64_t len : lens) {
@@ -205,19 +214,21 @@ std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles
     units.push(t);
     makespan = std::max(makespan, t);
   }
-  if (makespan <= limit) return cuts;
+  if (makespan <= limit) return;
   // The same schedule with cuts.
   while (!units.empty()) units.pop();
   for (int u = 0; u < n_units; ++u) units.push(0);
-  for (size_t i = 0; i < tiles.size(); ++i)
-    if (tiles[i] > 0) queue.push(Seg{tiles[i], (int32_t)i, 0});
+  auto longer = [](const Seg& a, const Seg& b) { return a.len < b.len || (a.len == b.len && a.item > b.item); };
+  std::priority_queue<Seg, std::vector<Seg>, decltype(longer)> queue(longer);
+  for (const ItemTiles& it : items) queue.push(Seg{it.tiles, it.item, 0});
   while (!queue.empty()) {
     const Seg s = queue.top();
     queue.pop();
     const int64_t load = units.top();
     units.pop();
     int64_t take = s.len;
-    if (load + s.len + kItemSetupTiles > limit && (int64_t)cuts[s.item].size() + 1 < kMaxPieces) {
+    const size_t n_cuts = cuts->empty() ? 0 : (*cuts)[(size_t)s.item].size();
+    if (load + s.len + kItemSetupTiles > limit && (int64_t)n_cuts + 1 < kMaxPieces) {
       // Fill this unit up to the ideal, or give it the smallest piece when
       // it is there already.
       const int64_t room = ideal - load - kItemSetupTiles;
@@ -225,12 +236,13 @@ std::vector<std::vector<int32_t>> balance_cuts(const std::vector<int64_t>& tiles
     }
     units.push(load + take + kItemSetupTiles);
     if (take < s.len) {
-      cuts[s.item].push_back(s.t0 + (int32_t)take);
+      if (cuts->empty()) cuts->resize(n_items_total);
+      (*cuts)[(size_t)s.item].push_back(s.t0 + (int32_t)take);
       queue.push(Seg{s.len - take, s.item, s.t0 + (int32_t)take});
     }
   }
-  for (auto& c : cuts) std::sort(c.begin(), c.end());
-  return cuts;
+  for (const ItemTiles& it : items)
+    if (!cuts->empty()) std::sort((*cuts)[(size_t)it.item].begin(), (*cuts)[(size_t)it.item].end());
 }
 
 // Key tiles of one work item's walk, exactly as the kernel counts them: the
@@ -308,14 +320,13 @@ int plan_items(int32_t Hq, int32_t Hkv, int rows, int64_t target_pieces, Plan* o
     // (the interleave below moves items between XCDs) and one schedule over
     // all of them is the closer model.
     const int n_sched = n_groups % kXcds == 0 ? kXcds : 1;
-    cuts.resize(blocks.size() * n_groups);
+    std::vector<ItemTiles> sched;
     for (int x = 0; x < n_sched; ++x) {
-      std::vector<int64_t> tiles(blocks.size() * n_groups, 0);
+      sched.clear();
       for (size_t bi = 0; bi < blocks.size(); ++bi)
-        for (int g = x; g < n_groups; g += n_sched) tiles[bi * n_groups + g] = blocks[bi].tiles;
-      const std::vector<std::vector<int32_t>> c = balance_cuts(tiles, kComputeUnits / n_sched);
-      for (size_t i = 0; i < c.size(); ++i)
-        if (!c[i].empty()) cuts[i] = c[i];
+        if (blocks[bi].tiles > 0)
+          for (int g = x; g < n_groups; g += n_sched) sched.push_back(ItemTiles{(int64_t)(bi * n_groups + g), blocks[bi].tiles});
+      balance_cuts(sched, kComputeUnits / n_sched, blocks.size() * n_groups, &cuts);
     }
   }
   out->splits.clear();
@@ -399,6 +410,40 @@ double estimate_us(const Plan& plan) {
   return makespan;
 }
 
+// Bounds (microseconds) of one shape's schedule before any item is cut: the
+// launch's work spread evenly over the compute units (every XCD gets the same
+// share of each block when the head groups are a multiple of the XCDs, and the
+// interleave spreads them otherwise), and that plus the longest item (list
+// scheduling ends within one item of the even spread).
+// `splits` tells whether the launch has few enough items to be split for
+// occupancy, which the bounds do not model.
+struct Bounds {
+  double lo, hi;
+  bool splits;
+};
+
+Bounds shape_bounds(const std::vector<DevDesc>& descs, int32_t Hq, int32_t Hkv, int rows) {
+  const Shape sh = shape_for(Hq, Hkv, rows);
+  const int n_groups = Hkv * sh.groups_per_kv;
+  const double tile_us = rows == kRowsLarge ? kSmallTileUs * 1.5 / kLargeTileGain : kSmallTileUs;
+  double work = 0.0;  // microseconds over all items
+  int64_t nonempty = 0, max_tiles = 0;
+  for (const DevDesc& d : descs)
+    for (int c = 0; c < 2; ++c)
+      for (int64_t qb = 0; qb * sh.q_per_wg < d.q_len[c]; ++qb) {
+        const int64_t tiles = item_tiles(d, c, qb, sh.q_per_wg);
+        work += (tiles * tile_us + kItemSetupUs) * n_groups;
+        if (tiles > 0) nonempty += n_groups;
+        max_tiles = std::max(max_tiles, tiles);
+      }
+  const double lo = work / kComputeUnits;
+  Bounds b;
+  b.lo = lo;
+  b.hi = lo + max_tiles * tile_us + kItemSetupUs;
+  b.splits = nonempty < kSplitBelowItems;
+  return b;
+}
+
 // Work-group shape forced by cp_set_workgroup_rows (0: chosen per launch).
 std::atomic<int> g_forced_rows{0};
 
@@ -431,6 +476,14 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
   // and keep the one whose simulated schedule ends first.
   const int forced = g_forced_rows.load();
   if (forced) return plan_items(Hq, Hkv, forced, target_pieces, out);
+  // When the bounds already decide (one shape's worst case ends before the
+  // other's best), only the winner is planned.
+  const Bounds bs = shape_bounds(out->descs, Hq, Hkv, kRowsSmall);
+  const Bounds bl = shape_bounds(out->descs, Hq, Hkv, kRowsLarge);
+  if (!bs.splits && !bl.splits) {
+    if (bl.hi < bs.lo) return plan_items(Hq, Hkv, kRowsLarge, target_pieces, out);
+    if (bs.hi < bl.lo) return plan_items(Hq, Hkv, kRowsSmall, target_pieces, out);
+  }
   Plan small;
   small.descs = out->descs;
   st = plan_items(Hq, Hkv, kRowsSmall, target_pieces, &small);
