@@ -133,11 +133,20 @@ def _check_workload(name, rank, n_random, block_every=1):
     return compare(f64(out[at]), f64(out_lse[at]), O_ref, L_ref, f"{name} rank {rank} pass-KV")
 
 
-def test_llama3_8b_32k_rank0_full_size():
-    _check_workload("llama3_8b_32k_c4", 0, n_random=24)
+@pytest.fixture(params=[0, 256, 384], ids=["rows_auto", "rows256", "rows384"])
+def workgroup_rows(request):
+    """The launch's own choice of workgroup shape, then each shape pinned (the
+    32K rank-0 shard in 384-row items is the one whose work list is cut)."""
+    cp.set_workgroup_rows(request.param)
+    yield request.param
+    cp.set_workgroup_rows(0)
 
 
-def test_llama3_8b_32k_rank3_full_size():
+def test_llama3_8b_32k_rank0_full_size(workgroup_rows):
+    _check_workload("llama3_8b_32k_c4", 0, n_random=24 if workgroup_rows == 0 else 8)
+
+
+def test_llama3_8b_32k_rank3_full_size(workgroup_rows):
     _check_workload("llama3_8b_32k_c4", 3, n_random=8)
 
 
@@ -154,7 +163,8 @@ CALIBRATION = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__fil
                            "calibration_attention_llama3_8b.json")
 
 
-def test_heterogeneous_batch_one_launch():
+@pytest.mark.parametrize("wg_rows", [0, 256, 384])
+def test_heterogeneous_batch_one_launch(wg_rows):
     """The heterogeneous mix (64 lognormal-length requests, 19 with a cached
     prefix in one shared paged pool) plus two long requests (40K tokens, and
     70K with a 16K cached prefix), each request at the CP degree the placement
@@ -191,9 +201,13 @@ def test_heterogeneous_batch_one_launch():
                                       pre.block_table if pre else None, include_prefix=True))
             keep.append((q, o, l))
             checks.append((ri, C, P, R, r, plan, rows, q, k, v, pre, o, l))
-    ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=DEV)
-    cp.attn_partial(descs, Hq, Hkv, ws)
-    torch.cuda.synchronize()
+    try:
+        cp.set_workgroup_rows(wg_rows)
+        ws = torch.empty(max(256, cp.workspace_size(descs, Hq, Hkv)), dtype=torch.uint8, device=DEV)
+        cp.attn_partial(descs, Hq, Hkv, ws)
+        torch.cuda.synchronize()
+    finally:
+        cp.set_workgroup_rows(0)
     kp, vp = f64(k_pool), f64(v_pool)
     rng = np.random.default_rng(7)
     n_rows = 0
