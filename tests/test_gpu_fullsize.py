@@ -9,10 +9,11 @@ and restored by cp_attn_merge with the rank's plan.
 The oracle recomputes seeded samples of rows (every head): the first and
 last rows of each chunk, rows on both sides of 64- and 256-row boundaries,
 random rows, and one seeded row in every 32-row block of each chunk (every
-8th block at the largest size) -- a wave owns 48 consecutive positions of
-one head, so every wave of every work item of the launch meets the oracle
-(at the largest size, where an item holds 48 positions of eight heads, one
-item in five or six).  Both steps' rows are compared with it.
+8th block at the largest size) -- a wave owns 32 or 48 consecutive
+positions of one head (256- or 384-row workgroups), so every wave of every
+work item of the launch meets the oracle (at the largest size, where an
+item holds 32 or 48 positions of eight heads, one item in five to eight).
+Both steps' rows are compared with it.
 Properties that hold at any size are checked on every row: the two steps
 agree, no NaN anywhere, and every restored row is written exactly once.
 """
