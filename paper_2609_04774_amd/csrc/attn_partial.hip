@@ -429,8 +429,9 @@ __device__ __forceinline__ void tile_limits(const Tile& x, int q0, bool wave_act
 // other's matrix work runs.
 //
 // Units: 4 NB times (two exponentials, one pack-and-sum) for score pairs,
-// against the running max (see kMaxTileSum).  The overflow check, and the
-// exact redo of a tile in the rare case that it fails, follow the region.
+// against the running max (see kMaxTileSum), in the order of kUnitOrder
+// below.  The overflow check, and the exact redo of a tile in the rare case
+// that it fails, follow the region.
 constexpr int kSlots = 16;
 template <int NB>
 constexpr int kLookahead = NB == 2 ? 3 : 2;
@@ -468,12 +469,46 @@ __device__ __forceinline__ void pack_and_sum(int b, int t, const Scores<NB>& s, 
   pin(pp);
 }
 
-// Unit u: pair t = (u / 3) % 4 of block b = u / 12; kind u % 3 (0, 1: one
-// exponential each; 2: pack and sum).
+// The order of the units: the exponentials of every block but the last
+// come first, then, once slot 8 starts (after the region's last use of the
+// previous P), the pack-and-sums, the last block's units interleaved with
+// its packs.  Each block's bf16 pairs are thereby produced after the
+// registers of its previous P are free, and land in them directly.
+struct Unit {
+  int b, t, kind;  // block, pair, kind (0, 1: one exponential each; 2: pack and sum)
+};
+template <int NB>
+struct UnitOrder {
+  Unit u[12 * NB];
+  constexpr UnitOrder() : u{} {
+    int n = 0;
+    for (int b = 0; b + 1 < NB; ++b)
+      for (int t = 0; t < 4; ++t)
+        for (int k = 0; k < 2; ++k) u[n++] = Unit{b, t, k};
+    const int last = NB - 1;
+    int te = 0;  // the last block's pairs whose exponentials are placed
+    for (; n < 6 * NB; ++te) {
+      u[n++] = Unit{last, te, 0};
+      u[n++] = Unit{last, te, 1};
+    }
+    for (int b = 0; b + 1 < NB; ++b)
+      for (int t = 0; t < 4; ++t) u[n++] = Unit{b, t, 2};
+    for (int t = 0; t < 4; ++t) {
+      if (t >= te) {
+        u[n++] = Unit{last, t, 0};
+        u[n++] = Unit{last, t, 1};
+      }
+      u[n++] = Unit{last, t, 2};
+    }
+  }
+};
+template <int NB>
+constexpr UnitOrder<NB> kUnitOrder{};
+
 template <int NB>
 __device__ __forceinline__ void softmax_unit(int u, Scores<NB>& s, SoftmaxState<NB>& st, const float (&m_run)[NB],
                                              float sl2) {
-  const int b = u / 12, t = (u / 3) % 4, kind = u % 3;
+  const int b = kUnitOrder<NB>.u[u].b, t = kUnitOrder<NB>.u[u].t, kind = kUnitOrder<NB>.u[u].kind;
   if (kind < 2) {
     const int kb = t >> 1, r = 2 * (t & 1) + kind;
     const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][b][r], sl2, -m_run[b]));
@@ -797,12 +832,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
       u32x4{};
   __syncthreads();  // the first tile is in LDS for everyone
   // A tile needs masking exactly when its index lies in [mA, firstB),
-  // [mB, firstC) or [mC, n) (the thresholds below).
+  // [mB, firstC) or [mC, n) (the thresholds below).  The tests between
+  // regions (mask, cursor, overflow) are marked with their common outcome so
+  // that it falls through: a taken branch costs the wave a fresh instruction
+  // fetch, about 1 % of the launch.
   auto masked_tile = [&](int j) {
-    return (j >= mask_a && j < tw.firstB) || (j >= mask_b && j < tw.firstC) || j >= mask_c;
+    return ((j >= mask_a) & (j < tw.firstB)) | ((j >= mask_b) & (j < tw.firstC)) | (j >= mask_c);
   };
   auto mask_if_needed = [&](int j, Scores<NB>& s) {
-    if (masked_tile(j)) {
+    if (__builtin_expect(masked_tile(j), 0)) {
       int lim[NB];
       tile_limits(tile_at(tw, j), q0, wave_active, wave_hi, qrel_b, valid_b, lim);
       mask_tile(s, g4, lim);
@@ -831,7 +869,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
   auto next_load = [&](int j) {
     const int t = j + kAhead, buf = t & (kBufs - 1);
     TileLoad ld;
-    if (t >= cur_full) {
+    if (__builtin_expect(t >= cur_full, 0)) {
       ld = load_of(t, buf);
       cur_full = next_full(t);
     } else {
@@ -857,7 +895,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_partial_kernel(const DevD
     bool ok = true;
 #pragma unroll
     for (int b = 0; b < NB; ++b) ok = ok && st.rs[b] <= kMaxTileSum;
-    if (__builtin_amdgcn_ballot_w64(!ok) != 0) {
+    if (__builtin_expect(__builtin_amdgcn_ballot_w64(!ok) != 0, 0)) {
       qk_tile(smem + B * kTileBytes, fo, qf, s_in);
       mask_if_needed(j, s_in);
       exact_softmax(s_in, m_run, l_run, psum, o, sl2, st);
