@@ -170,65 +170,65 @@ constexpr double kBalanceSlack = 1.03;
 // last round of long items runs on a few units while the rest idle.  This
 // simulates that schedule (item time = its tiles + kItemSetupTiles) and, when
 // its makespan exceeds the ideal (total / units) by more than kBalanceSlack,
-// replays it cutting items: an item that would push the least loaded unit
-// past the ideal gives that unit only the tiles that fill it up, and its
-// remaining tiles go back into the queue as a later item.  Both parts of a
-// cut keep at least kMinBalancePiece tiles (every piece costs a set-up, and
-// its rows a merge).  Returns each item's interior cut points (tile indices,
+// tries two ways of cutting items into pieces:
+//  * fill: the same schedule, where an item that would push the least loaded
+//    unit past the ideal gives that unit only the tiles that fill it up, its
+//    remaining tiles going back into the queue as a later item;
+//  * even: the longest items are placed whole while the least loaded unit
+//    takes them within the bound; each item left that can be cut in two is
+//    cut into equal pieces, m units' worth of pieces in all (m = 1 .. 4),
+//    dealt in proportion to the items' lengths.
+// Each candidate is scored by the schedule that the dispatch makes of it (all
+// pieces sorted longest first), and the one that ends first is kept; fewer
+// pieces win a tie.  Every piece keeps at least kMinBalancePiece tiles (each
+// costs a set-up, and its rows a merge).  Fill suits a few long items over a
+// round of shorter ones (the 32K prompt's rank 0, whose short chunk's items
+// fill the gaps); even suits rounds of equally long items (a prompt behind a
+// long cached prefix), where fill's remainders are too long for the room
+// they find.  Returns each item's interior cut points (tile indices,
 // ascending) in `cuts` (indexed by the items' numbers, allocated only when a
-// cut is made); nothing when no cut pays.
+// cut is made).
 struct ItemTiles {
   int64_t item;   // the item's number in the launch
   int64_t tiles;  // its key walk
 };
 
-void balance_cuts(const std::vector<ItemTiles>& items, int n_units, size_t n_items_total,
-                  std::vector<std::vector<int32_t>>* cuts) {
-  struct Seg {
-    int64_t len;
-    int64_t item;
-    int32_t t0;
-  };
-  int64_t total = 0, longest = 0;
-  for (const ItemTiles& it : items) {
-    total += it.tiles + kItemSetupTiles;
-    longest = std::max(longest, it.tiles);
-  }
-  if (items.empty()) return;
-  const int64_t ideal = (total + n_units - 1) / n_units;
-  const int64_t limit = (int64_t)(ideal * kBalanceSlack);
-  // List scheduling ends within one item of the even spread: when the longest
-  // item fits in the slack, no schedule needs cuts (and none is simulated).
-  if (ideal + longest + kItemSetupTiles <= limit) return;
-  // The schedule without cuts.
-  std::vector<int64_t> lens;
-  lens.reserve(items.size());
-  for (const ItemTiles& it : items) lens.push_back(it.tiles);
-  std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
-  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
-  for (int u = 0; u < n_units; ++u) units.push(0);
-  int64_t makespan = 0;
+// Makespan of list scheduling `lens` (sorted longest first) onto units whose
+// loads start at `loads`.
+int64_t list_schedule(const std::vector<int64_t>& loads, const std::vector<int64_t>& lens) {
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units(loads.begin(), loads.end());
+  int64_t makespan = *std::max_element(loads.begin(), loads.end());
   for (int64_t len : lens) {
     const int64_t t = units.top() + len + kItemSetupTiles;
     units.pop();
     units.push(t);
     makespan = std::max(makespan, t);
   }
-  if (makespan <= limit) return;
-  // The same schedule with cuts.
-  while (!units.empty()) units.pop();
+  return makespan;
+}
+
+typedef std::vector<std::vector<int32_t>> Cuts;  // per item (position in the list): cut points
+
+// The fill candidate (see balance_cuts).
+Cuts fill_cuts(const std::vector<ItemTiles>& items, int n_units, int64_t ideal, int64_t limit) {
+  struct Seg {
+    int64_t len;
+    size_t idx;
+    int32_t t0;
+  };
+  Cuts c(items.size());
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
   for (int u = 0; u < n_units; ++u) units.push(0);
-  auto longer = [](const Seg& a, const Seg& b) { return a.len < b.len || (a.len == b.len && a.item > b.item); };
+  auto longer = [](const Seg& a, const Seg& b) { return a.len < b.len || (a.len == b.len && a.idx > b.idx); };
   std::priority_queue<Seg, std::vector<Seg>, decltype(longer)> queue(longer);
-  for (const ItemTiles& it : items) queue.push(Seg{it.tiles, it.item, 0});
+  for (size_t i = 0; i < items.size(); ++i) queue.push(Seg{items[i].tiles, i, 0});
   while (!queue.empty()) {
     const Seg s = queue.top();
     queue.pop();
     const int64_t load = units.top();
     units.pop();
     int64_t take = s.len;
-    const size_t n_cuts = cuts->empty() ? 0 : (*cuts)[(size_t)s.item].size();
-    if (load + s.len + kItemSetupTiles > limit && (int64_t)n_cuts + 1 < kMaxPieces) {
+    if (load + s.len + kItemSetupTiles > limit && (int64_t)c[s.idx].size() + 1 < kMaxPieces) {
       // Fill this unit up to the ideal, or give it the smallest piece when
       // it is there already.
       const int64_t room = ideal - load - kItemSetupTiles;
@@ -236,13 +236,115 @@ void balance_cuts(const std::vector<ItemTiles>& items, int n_units, size_t n_ite
     }
     units.push(load + take + kItemSetupTiles);
     if (take < s.len) {
-      if (cuts->empty()) cuts->resize(n_items_total);
-      (*cuts)[(size_t)s.item].push_back(s.t0 + (int32_t)take);
-      queue.push(Seg{s.len - take, s.item, s.t0 + (int32_t)take});
+      c[s.idx].push_back(s.t0 + (int32_t)take);
+      queue.push(Seg{s.len - take, s.idx, s.t0 + (int32_t)take});
     }
   }
-  for (const ItemTiles& it : items)
-    if (!cuts->empty()) std::sort((*cuts)[(size_t)it.item].begin(), (*cuts)[(size_t)it.item].end());
+  for (std::vector<int32_t>& v : c) std::sort(v.begin(), v.end());
+  return c;
+}
+
+// The even candidate for m units' worth of pieces (see balance_cuts); no cut
+// when it makes none.
+Cuts even_cuts(const std::vector<ItemTiles>& items, int n_units, int64_t limit, int m) {
+  Cuts c(items.size());
+  std::vector<size_t> order(items.size());
+  for (size_t i = 0; i < items.size(); ++i) order[i] = i;
+  std::sort(order.begin(), order.end(), [&](size_t a, size_t b) {
+    return items[a].tiles > items[b].tiles || (items[a].tiles == items[b].tiles && a < b);
+  });
+  // The longest items, each while the least loaded unit takes it within the
+  // limit.
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> units;
+  for (int u = 0; u < n_units; ++u) units.push(0);
+  size_t n_whole = 0;
+  for (; n_whole < order.size(); ++n_whole) {
+    const int64_t t = units.top() + items[order[n_whole]].tiles + kItemSetupTiles;
+    if (t > limit) break;
+    units.pop();
+    units.push(t);
+  }
+  std::vector<size_t> big;  // the rest that can be cut in two
+  int64_t big_tiles = 0;
+  for (size_t k = n_whole; k < order.size(); ++k)
+    if (items[order[k]].tiles >= 2 * kMinBalancePiece) {
+      big.push_back(order[k]);
+      big_tiles += items[order[k]].tiles;
+    }
+  const int64_t target = (int64_t)m * n_units;
+  if (target <= (int64_t)big.size()) return c;
+  // Pieces in proportion to the lengths (largest remainders first), each
+  // item's at most its length allows.
+  std::vector<int64_t> n_pieces(big.size());
+  std::vector<std::pair<double, size_t>> frac;
+  int64_t dealt = 0;
+  for (size_t i = 0; i < big.size(); ++i) {
+    const int64_t len = items[big[i]].tiles;
+    const double share = (double)target * (double)len / (double)big_tiles;
+    const int64_t most = std::min<int64_t>(kMaxPieces, len / kMinBalancePiece);
+    n_pieces[i] = std::max<int64_t>(1, std::min<int64_t>(most, (int64_t)share));
+    dealt += n_pieces[i];
+    if (n_pieces[i] < most) frac.push_back(std::make_pair(share - (double)n_pieces[i], i));
+  }
+  std::stable_sort(frac.begin(), frac.end(), [](const std::pair<double, size_t>& x, const std::pair<double, size_t>& y) {
+    return x.first > y.first;
+  });
+  for (size_t f = 0; f < frac.size() && dealt < target; ++f, ++dealt) ++n_pieces[frac[f].second];
+  for (size_t i = 0; i < big.size(); ++i) {
+    const int64_t len = items[big[i]].tiles;
+    for (int64_t k = 1; k < n_pieces[i]; ++k) c[big[i]].push_back((int32_t)(len * k / n_pieces[i]));
+  }
+  return c;
+}
+
+// The dispatch's schedule of a candidate: makespan and piece count.
+std::pair<int64_t, int64_t> score_cuts(const std::vector<ItemTiles>& items, const Cuts& c, int n_units) {
+  std::vector<int64_t> lens;
+  int64_t pieces = 0;
+  for (size_t i = 0; i < items.size(); ++i) {
+    int32_t prev = 0;
+    for (int32_t x : c[i]) {
+      lens.push_back(x - prev);
+      prev = x;
+    }
+    lens.push_back(items[i].tiles - prev);
+    if (!c[i].empty()) pieces += (int64_t)c[i].size() + 1;
+  }
+  std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
+  return std::make_pair(list_schedule(std::vector<int64_t>(n_units, 0), lens), pieces);
+}
+
+void balance_cuts(const std::vector<ItemTiles>& items, int n_units, size_t n_items_total, Cuts* cuts) {
+  if (items.empty()) return;
+  int64_t total = 0, longest = 0;
+  for (const ItemTiles& it : items) {
+    total += it.tiles + kItemSetupTiles;
+    longest = std::max(longest, it.tiles);
+  }
+  const int64_t ideal = (total + n_units - 1) / n_units;
+  const int64_t limit = (int64_t)(ideal * kBalanceSlack);
+  // List scheduling ends within one item of the even spread: when the longest
+  // item fits in the slack, no schedule needs cuts (and none is simulated).
+  if (ideal + longest + kItemSetupTiles <= limit) return;
+  const Cuts none(items.size());
+  std::pair<int64_t, int64_t> best = score_cuts(items, none, n_units);
+  if (best.first <= limit) return;
+  Cuts chosen;
+  auto consider = [&](Cuts c) {
+    const std::pair<int64_t, int64_t> sc = score_cuts(items, c, n_units);
+    if (sc.first < best.first || (sc.first == best.first && sc.second < best.second)) {
+      best = sc;
+      chosen.swap(c);
+    }
+  };
+  consider(fill_cuts(items, n_units, ideal, limit));
+  for (int m = 1; m <= 4; ++m) consider(even_cuts(items, n_units, limit, m));
+  if (chosen.empty()) return;
+  for (size_t i = 0; i < items.size(); ++i) {
+    if (chosen[i].empty()) continue;
+    if (cuts->empty()) cuts->resize(n_items_total);
+    (*cuts)[(size_t)items[i].item] = chosen[i];
+  }
 }
 
 // Key tiles of one work item's walk, exactly as the kernel counts them: the

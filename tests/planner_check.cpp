@@ -7,7 +7,8 @@
 //     key walk [0, tiles) in order, one slot per piece, described by exactly
 //     one split item;
 //   * pieces keep the minimum sizes of their policy (at least 32 tiles when a
-//     launch with few items is split for occupancy, 256 for balance cuts);
+//     launch with few items is split for occupancy, 256 for balance cuts,
+//     whether they fill units up or cut items evenly);
 //   * the work list holds nothing else, and the workspace layout holds one
 //     slot of the shape's size per piece.
 // Prints "ok <cases>" on success, else the first failure, and exits non-zero.
@@ -163,6 +164,25 @@ int main() {
   expect(!p.splits.empty(), "32K rank 0 in 384-row items has no balance cuts");
   for (const WorkItem& w : p.items)
     if (w.piece >= 0) expect(w.t_end - w.t_begin >= kMinBalancePiece, "balance piece below 256 tiles");
+  // A prompt behind a long cached prefix (every item about equally long, 2.7
+  // per compute unit in 384-row items) is cut into even pieces: more than
+  // the fill cuts' one per item left over, none below 256 tiles, and the
+  // dispatch's schedule within 3 % of the even spread.
+  const cp_partial_desc dp = desc(49152, 16384, 2, 0, CP_KV_ALL, 1);
+  build_plan(&dp, 1, 32, 8, kTargetPieces, &p);
+  expect(p.n_pieces > 352, "prefix launch in 384-row items should be cut evenly");
+  int64_t work = 0;
+  std::vector<int64_t> lens;
+  for (const WorkItem& w : p.items) {
+    const int64_t t = w.piece >= 0 ? w.t_end - w.t_begin : item_tiles(p.descs[w.desc], w.chunk, w.q_block, p.shape.q_per_wg);
+    if (w.piece >= 0) expect(t >= kMinBalancePiece, "even piece below 256 tiles");
+    work += t + kItemSetupTiles;
+    lens.push_back(t);
+  }
+  std::sort(lens.begin(), lens.end(), std::greater<int64_t>());
+  const int64_t spread = work / kComputeUnits;
+  expect(list_schedule(std::vector<int64_t>(kComputeUnits, 0), lens) <= spread * 103 / 100,
+         "prefix launch's schedule more than 3 % past the even spread");
   // The per-launch choice keeps 384 rows for that launch and 256 for few
   // long walks.
   cp_set_workgroup_rows(0);
