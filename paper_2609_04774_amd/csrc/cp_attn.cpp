@@ -481,11 +481,13 @@ int plan_items(int32_t Hq, int32_t Hkv, int rows, int64_t target_pieces, Plan* o
 // of its work list simulated on each XCD's 32 compute units (list item i on
 // XCD i % 8), an item taking its tiles times the shape's time per tile plus
 // a fixed set-up, then the split merge's traffic.  The 384-row shape's tile
-// is 1.5 times the 256-row one's work at kLargeTileGain times its rate (the
-// two kernels timed on launches that both balance).
-constexpr double kSmallTileUs = 0.93;   // a 256-row x 32-key tile on one compute unit
-constexpr double kLargeTileGain = 1.08;
-constexpr double kItemSetupUs = 4.0;
+// is 1.5 times the 256-row one's work at kLargeTileGain times its rate.  The
+// three constants are fitted to both shapes' times on 136 rank launches (the
+// prompts of 4K-32K tokens at C = 1-8 with and without a 16K prefix, and five
+// larger shapes), timed alternately in one process.
+constexpr double kSmallTileUs = 0.90;   // a 256-row x 32-key tile on one compute unit
+constexpr double kLargeTileGain = 1.06;
+constexpr double kItemSetupUs = 8.0;
 constexpr double kMergeBytesPerUs = 5.0e6;
 
 double estimate_us(const Plan& plan) {
