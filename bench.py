@@ -72,11 +72,13 @@ def parse():
 def profiled_figures(workload, mode="allgather"):
     """Figures of the committed counter profile of this workload's launch in
     this mode (HBM bytes per attention launch, and where recorded the clock
-    and MFMA-busy fraction), if the kernel source is still the one that was
-    profiled."""
+    and MFMA-busy fraction), if the kernel and planner sources are still the
+    ones that were profiled (the plan decides which items are cut, and the
+    pieces' partials are traffic too)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{mode}.txt")
     src = os.path.join(ROOT, "paper_2609_04774_amd", "csrc", "attn_partial.hip")
+    planner = os.path.join(ROOT, "paper_2609_04774_amd", "csrc", "cp_attn.cpp")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -87,7 +89,11 @@ def profiled_figures(workload, mode="allgather"):
             kv[key] = val
     with open(src, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
-    if kv.get("kernel_source_sha256") != sha or kv.get("mode") != mode:
+    with open(planner, "rb") as f:
+        planner_sha = hashlib.sha256(f.read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha or kv.get("planner_source_sha256") != planner_sha:
+        return None
+    if kv.get("mode") != mode:
         return None
     out = {"traffic": int(kv["fetch_bytes"]) + int(kv["write_bytes"])}
     if "clock_ghz" in kv and "mfma_busy" in kv:
