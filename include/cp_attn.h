@@ -224,9 +224,10 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
  *               this work.
  * Each call stages the descriptor copy through pinned host memory owned by
  * the library (allocated on first use, kept until process exit), in a ring
- * of eight slots: a call that finds its slot's previous copy not yet done
- * blocks the calling host thread on that copy's event (never on the whole
- * device) before reusing the slot.
+ * of eight slots, and a small kernel on `stream` copies it into the
+ * workspace: a call that finds its slot's previous copy not yet done blocks
+ * the calling host thread on that copy's event (never on the whole device)
+ * before reusing the slot.
  * Errors: CP_ERR_INVALID (shapes, plans, pointers, alignment, kv_rank),
  * CP_ERR_UNSUPPORTED (head_dim; a request with P + R > 2^30 tokens),
  * CP_ERR_CAPACITY (workspace), CP_ERR_HIP.

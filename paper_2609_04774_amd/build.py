@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 ARCH = "gfx950"
 
 SOURCES = ["plan.cpp", "cp_attn.cpp", "noalloc.cpp", "kv_cache.cpp", "attn_partial.hip", "lse_merge.hip",
-           "kv_cache.hip"]
+           "kv_cache.hip", "upload.hip"]
 
 # Packed-FP32 VALU forms are kept out of every kernel (-packed-fp32-ops).
 HIP_FLAGS = [

@@ -642,10 +642,13 @@ PartialParams partial_params(const Plan& plan, const Layout& lay, unsigned char*
 
 namespace {
 
-// Pinned host staging for the descriptor/work-list upload.  A slot is reused
-// only after the copy that read it has completed (its event).
+// Pinned host staging for the descriptor/work-list upload, mapped into the
+// device's address space and coherent (the device reads it over the bus,
+// never from a cached copy): the upload kernel reads it (upload.hip).  A slot
+// is reused only after the upload that read it has completed (its event).
 struct Slot {
   void* host = nullptr;
+  void* mapped = nullptr;  // the same memory as the device addresses it
   size_t cap = 0;
   hipEvent_t ev = nullptr;
   int device = -1;
@@ -680,15 +683,18 @@ int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream)
   if (s.cap < bytes) {
     if (s.host) (void)hipHostFree(s.host);
     s.host = nullptr;
+    s.mapped = nullptr;
     s.cap = 0;
     const size_t cap = std::max<size_t>(bytes, 64 * 1024);
-    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    e = hipHostMalloc(&s.host, cap, hipHostMallocMapped | hipHostMallocPortable | hipHostMallocCoherent);
     if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipHostMalloc (staging): ") + hipGetErrorString(e));
+    e = hipHostGetDevicePointer(&s.mapped, s.host, 0);
+    if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipHostGetDevicePointer (staging): ") + hipGetErrorString(e));
     s.cap = cap;
   }
   std::memcpy(s.host, src, bytes);
-  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipMemcpyAsync (descriptors): ") + hipGetErrorString(e));
+  const int up = cpattn::launch_upload(dst, s.mapped, bytes, stream);
+  if (up != CP_OK) return up;
   e = hipEventRecord(s.ev, stream);
   if (e != hipSuccess) return fail(CP_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
   s.pending = true;

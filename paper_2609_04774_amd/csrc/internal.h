@@ -129,6 +129,11 @@ struct PartialParams {
 
 int launch_partial(const PartialParams& p, void* stream);
 
+// Copies `bytes` (a multiple of 16) from pinned host memory mapped into the
+// device's address space to device memory, with a kernel on `stream`
+// (upload.hip).
+int launch_upload(void* dst, const void* src, size_t bytes, void* stream);
+
 // Host planning of one cp_attn_partial launch (cp_attn.cpp), shared by the
 // entry points that take a caller workspace and the one that uses the
 // library's own scratch.
