@@ -210,7 +210,7 @@ def counter_profile(workload, args, rank, frac):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build executes every CP rank's shard "
+        print("bench.py runs on exactly one GPU: the library executes every CP rank's shard "
               "on a single MI355X and has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
         sys.exit(2)
 

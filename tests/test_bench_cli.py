@@ -1,5 +1,5 @@
 """bench.py's command-line contract that can be checked without a GPU: more
-than one GPU is refused with a message (this build runs every rank's shard
+than one GPU is refused with a message (the library runs every rank's shard
 on one GPU), and the measured-traffic lookup only returns figures recorded
 for the kernel and planner sources as they are now."""
 
