@@ -1,7 +1,7 @@
 // Host-only check of the attention work list (tests/test_planner.py builds and
 // runs it; no GPU is touched).  It includes the planner's source so that the
-// internal plan can be inspected, builds the plan of several launches in each
-// workgroup shape and checks:
+// internal plan can be inspected, builds the plan of several launches (named
+// ones and 60 seeded random ones) in each workgroup shape and checks:
 //   * every (descriptor, chunk, query block, head group) of the launch is
 //     scheduled exactly once: whole, or as pieces whose tile ranges cover its
 //     key walk [0, tiles) in order, one slot per piece, described by exactly
@@ -148,6 +148,30 @@ int main() {
     for (int i = 0; i < 5; ++i)
       for (int r = 0; r < degrees[i]; ++r)
         l.descs.push_back(desc(lens[i][1], lens[i][0] - lens[i][1], degrees[i], r, CP_KV_ALL, 1));
+    launches.push_back(l);
+  }
+  // Random launches (fixed seed): prompts of 1..64K new tokens behind 0..64K
+  // cached ones, degree 1..8, one all-gathered partial or a rank's pass-KV
+  // partials, several head layouts.
+  uint64_t rng = 0x9e3779b97f4a7c15ULL;
+  auto next = [&](uint64_t n) {
+    rng ^= rng << 13;
+    rng ^= rng >> 7;
+    rng ^= rng << 17;
+    return (int64_t)(rng % n);
+  };
+  const int heads[][2] = {{32, 8}, {64, 8}, {12, 4}, {16, 16}, {8, 2}};
+  for (int i = 0; i < 60; ++i) {
+    const int C = 1 << next(4);
+    const int64_t R = 2 * C + next(65536 - 2 * C);
+    const int64_t P = 16 * next(4097);
+    const int rank = (int)next(C);
+    const int* h = heads[next(5)];
+    Launch l{"random " + std::to_string(i), {}, h[0], h[1]};
+    if (next(2))
+      l.descs.push_back(desc(P, R, C, rank, CP_KV_ALL, 1));
+    else
+      for (int sh = 0; sh < C; ++sh) l.descs.push_back(desc(P, R, C, rank, sh, sh == 0));
     launches.push_back(l);
   }
   int cases = 0;
