@@ -137,7 +137,8 @@ def _check_workload(name, rank, n_random, block_every=1):
 @pytest.fixture(params=[0, 256, 384], ids=["rows_auto", "rows256", "rows384"])
 def workgroup_rows(request):
     """The launch's own choice of workgroup shape, then each shape pinned (the
-    32K rank-0 shard in 384-row items is the one whose work list is cut)."""
+    32K rank-0 shard's work list is cut in 384-row items only; the prefix-hit
+    shard's, checked in its own choice of shape, is cut evenly)."""
     cp.set_workgroup_rows(request.param)
     yield request.param
     cp.set_workgroup_rows(0)
