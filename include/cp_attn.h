@@ -222,6 +222,11 @@ size_t cp_attn_partial_workspace_size(const cp_partial_desc* descs, int32_t n_de
  *               written by an asynchronous copy on `stream` and read by the
  *               kernel, so it must not be reused until the stream reaches
  *               this work.
+ * The work list is planned on the host; the lists of the last 16 launches
+ * are kept (keyed by every non-pointer field of the descriptors, the head
+ * counts and the pinned workgroup shape, matched exactly), so a launch of
+ * the same geometry with other buffers, such as the next layer's, reuses its
+ * list instead of planning it again.
  * Each call stages the descriptor copy through pinned host memory owned by
  * the library (allocated on first use, kept until process exit), in a ring
  * of eight slots, and a small kernel on `stream` copies it into the

@@ -563,6 +563,38 @@ extern "C" int cp_set_workgroup_rows(int32_t rows) {
 
 namespace cpattn {
 
+// Work lists of recent launches.  A layer after layer of the same shapes
+// plans the same list (the work list depends on the descriptors' positions,
+// chunks and key ranges and on the heads, never on their buffers), so the
+// list of a launch whose key matches is reused instead of planned again:
+// the key holds every non-pointer field of the converted descriptors, the
+// head counts, the piece target and the pinned shape, and matches exactly.
+struct CachedPlan {
+  std::vector<int64_t> key;
+  std::vector<WorkItem> items;
+  std::vector<SplitItem> splits;
+  int64_t n_pieces;
+  Shape shape;
+};
+constexpr size_t kPlanCacheSize = 16;
+static std::mutex g_plan_cache_mu;
+static std::vector<CachedPlan> g_plan_cache;  // most recent last
+static size_t g_plan_cache_hits = 0;
+
+static std::vector<int64_t> plan_key(const std::vector<DevDesc>& descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
+                                     int forced) {
+  std::vector<int64_t> k = {Hq, Hkv, target_pieces, forced, (int64_t)descs.size()};
+  for (const DevDesc& d : descs) {
+    const int64_t f[] = {d.P, d.R, d.q_begin[0], d.q_begin[1], d.q_len[0], d.q_len[1], d.local_off[0], d.local_off[1],
+                         d.o_off[0], d.o_off[1], d.seg_lo[0], d.seg_lo[1], d.seg_hi[0], d.seg_hi[1], d.n_seg,
+                         d.prefix_keys, d.n_blocks, d.reserved};
+    k.insert(k.end(), f, f + sizeof(f) / sizeof(f[0]));
+  }
+  return k;
+}
+
+static int plan_uncached(int32_t Hq, int32_t Hkv, int64_t target_pieces, int forced, Plan* out);
+
 int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_t Hkv, int64_t target_pieces,
                Plan* out) {
   int st = check_heads(Hq, Hkv, "cp_attn_partial");
@@ -574,11 +606,36 @@ int build_plan(const cp_partial_desc* descs, int32_t n_descs, int32_t Hq, int32_
     st = to_dev(descs[i], i, &out->descs[i]);
     if (st != CP_OK) return st;
   }
+  const int forced = g_forced_rows.load();
+  std::vector<int64_t> key = plan_key(out->descs, Hq, Hkv, target_pieces, forced);
+  {
+    std::lock_guard<std::mutex> lock(g_plan_cache_mu);
+    for (size_t i = g_plan_cache.size(); i-- > 0;) {
+      const CachedPlan& c = g_plan_cache[i];
+      if (c.key != key) continue;
+      out->items = c.items;
+      out->splits = c.splits;
+      out->n_pieces = c.n_pieces;
+      out->shape = c.shape;
+      ++g_plan_cache_hits;
+      return CP_OK;
+    }
+  }
+  st = plan_uncached(Hq, Hkv, target_pieces, forced, out);
+  if (st != CP_OK) return st;
+  std::lock_guard<std::mutex> lock(g_plan_cache_mu);
+  if (g_plan_cache.size() == kPlanCacheSize) g_plan_cache.erase(g_plan_cache.begin());
+  g_plan_cache.push_back(CachedPlan{std::move(key), out->items, out->splits, out->n_pieces, out->shape});
+  return CP_OK;
+}
+
+// The work list of a launch whose descriptors are converted (out->descs).
+static int plan_uncached(int32_t Hq, int32_t Hkv, int64_t target_pieces, int forced, Plan* out) {
+  int st;
   // The workgroup shape: two or three 16-row blocks per wave.  The larger
   // shares every K/V fragment between more rows (faster per tile) but makes
   // fewer, longer work items, which fill the compute units worse; plan both
   // and keep the one whose simulated schedule ends first.
-  const int forced = g_forced_rows.load();
   if (forced) return plan_items(Hq, Hkv, forced, target_pieces, out);
   // When the bounds already decide (one shape's worst case ends before the
   // other's best), only the winner is planned.

@@ -10,7 +10,9 @@
 //     launch with few items is split for occupancy, 256 for balance cuts,
 //     whether they fill units up or cut items evenly);
 //   * the work list holds nothing else, and the workspace layout holds one
-//     slot of the shape's size per piece.
+//     slot of the shape's size per piece;
+//   * a launch planned again is served from the plan cache with the list a
+//     fresh plan gives, and a launch that differs is planned anew.
 // Prints "ok <cases>" on success, else the first failure, and exits non-zero.
 #include "../paper_2609_04774_amd/csrc/cp_attn.cpp"
 
@@ -208,6 +210,38 @@ int main() {
   const int64_t spread = work / kComputeUnits;
   expect(list_schedule(std::vector<int64_t>(kComputeUnits, 0), lens) <= spread * 103 / 100,
          "prefix launch's schedule more than 3 % past the even spread");
+  // The plan cache: a launch planned again (its buffers moved) gets the work
+  // list that planning it afresh gives, from the cache; another rank, head
+  // layout or pinned shape is planned anew.
+  {
+    cp_set_workgroup_rows(0);
+    cp_partial_desc a = desc(16384, 16384, 4, 1, CP_KV_ALL, 1);
+    Plan first, again, fresh;
+    build_plan(&a, 1, 32, 8, kTargetPieces, &first);
+    a.q = a.k_new = reinterpret_cast<void*>(0x200000);  // other buffers, same geometry
+    const size_t hits = g_plan_cache_hits;
+    build_plan(&a, 1, 32, 8, kTargetPieces, &again);
+    expect(g_plan_cache_hits == hits + 1, "plan cache: an identical launch is not served from the cache");
+    expect(again.descs[0].q == reinterpret_cast<const uint16_t*>(0x200000), "plan cache: stale buffer pointers");
+    fresh.descs = again.descs;
+    plan_uncached(32, 8, kTargetPieces, 0, &fresh);
+    bool same = fresh.items.size() == again.items.size() && fresh.splits.size() == again.splits.size() &&
+                fresh.n_pieces == again.n_pieces && fresh.shape.rows_per_wg == again.shape.rows_per_wg;
+    for (size_t i = 0; same && i < fresh.items.size(); ++i)
+      same = std::memcmp(&fresh.items[i], &again.items[i], sizeof(WorkItem)) == 0;
+    for (size_t i = 0; same && i < fresh.splits.size(); ++i)
+      same = std::memcmp(&fresh.splits[i], &again.splits[i], sizeof(SplitItem)) == 0;
+    expect(same, "plan cache: the cached work list differs from a fresh plan");
+    const cp_partial_desc b2 = desc(16384, 16384, 4, 2, CP_KV_ALL, 1);
+    Plan other;
+    build_plan(&b2, 1, 32, 8, kTargetPieces, &other);
+    build_plan(&a, 1, 64, 8, kTargetPieces, &other);
+    cp_set_workgroup_rows(kRowsSmall);
+    build_plan(&a, 1, 32, 8, kTargetPieces, &other);
+    expect(g_plan_cache_hits == hits + 1, "plan cache: a different launch was served from the cache");
+    expect(other.shape.rows_per_wg == kRowsSmall, "plan cache: the pinned shape was not planned");
+    cp_set_workgroup_rows(0);
+  }
   // The per-launch choice keeps 384 rows for that launch and 256 for few
   // long walks.
   cp_set_workgroup_rows(0);
